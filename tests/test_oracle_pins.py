@@ -1,0 +1,466 @@
+"""Pins of the CPU oracle against what the paper and arithmetic fix.
+
+Each check is chosen so that a plausible slip in the oracle (a dropped tensor,
+a wrong split dim, a transposed box, a wrong sender, a wrong matrix
+orientation) fails at least one of them."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import (ESIZE, empty_arenas, full_cols, host_arenas, lcm, rank_elems, send_bufs,
+                     unique_params)
+from micro import MICRO_MODELS, cfg_pairs, layers_only
+from paper_2607_04749_amd.workloads import GPT, WORKLOADS, Parallel
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    vals = {}
+    for line in open(os.path.join(GOLDEN, name)):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        k, *v = line.split()
+        vals[k] = [int(x) for x in v]
+    return vals
+
+
+# ---------------------------------------------------------------- the paper's example
+
+def test_paper_worked_example_pp4_to_pp2():
+    """Sec. III-B: 16 layers, PP 4 -> 2; c_00 = 4 layers; rows are the current
+    ranks, columns the previous ones."""
+    g = _golden("paper_pp4_to_pp2.txt")
+    model = layers_only(g["num_layers"][0])
+    prev, curr = Parallel(1, g["prev_pp"][0]), Parallel(1, g["curr_pp"][0])
+    # workloads of rank 0 on both sides
+    lp = {oracle.tensors(model)[p["tensor"]]["layer"] for p in oracle.layout(model, prev, 0)[0]}
+    lc = {oracle.tensors(model)[p["tensor"]]["layer"] for p in oracle.layout(model, curr, 0)[0]}
+    assert sorted(lp) == g["prev_rank0_layers"]
+    assert sorted(lc) == g["curr_rank0_layers"]
+    cost = oracle.matrices(model, prev, curr)["cost"]
+    assert cost.shape == (2, 4)  # M = curr ranks x N = prev ranks
+    h, f = model.hidden, model.ffn_hidden
+    layer_bytes = 14 * (4 * h * h + 2 * f * h + 9 * h + f)
+    assert cost[0, 0] == g["c_0_0"][0] * layer_bytes
+    # the rest of the matrix follows from the same definition
+    expect = np.array([[4, 4, 8, 8], [8, 8, 4, 4]], np.uint64) * layer_bytes
+    np.testing.assert_array_equal(cost, expect)
+
+
+def test_cost_matrix_orientation_not_square():
+    """PP 2 -> 4: C has 4 rows (current ranks) and 2 columns (previous)."""
+    model = layers_only(8)
+    cost = oracle.matrices(model, Parallel(1, 2), Parallel(1, 4))["cost"]
+    assert cost.shape == (4, 2)
+    h, f = model.hidden, model.ffn_hidden
+    lb = 14 * (4 * h * h + 2 * f * h + 9 * h + f)
+    np.testing.assert_array_equal(cost // lb, [[0, 2], [0, 2], [2, 0], [2, 0]])
+
+
+# ---------------------------------------------------------------- closed forms
+
+@pytest.mark.parametrize("wl", sorted(WORKLOADS))
+def test_rank_bytes_closed_form(wl):
+    """Column sums of ROUTE are the bytes each target rank holds; those equal
+    the architecture's parameter count split by the partition rules."""
+    w = WORKLOADS[wl]
+    M = oracle.matrices(w.model, w.src, w.dst)
+    for d in range(w.dst.world):
+        assert int(M["route"][:, d].sum()) == 14 * rank_elems(w.model, w.dst, d)
+        assert oracle.layout(w.model, w.dst, d)[1] >= rank_elems(w.model, w.dst, d)
+    for s in range(w.src.world):
+        held = sum((p["r1"] - p["r0"]) * (p["c1"] - p["c0"]) for p in oracle.layout(w.model, w.src, s)[0])
+        assert held == rank_elems(w.model, w.src, s)
+
+
+def test_tiny_totals():
+    """Tiny GPT: 3,454,464 unique parameters (GPT count 12h^2+13h per layer
+    with FFN 4h, plus embeddings and the final norm)."""
+    w = WORKLOADS["tiny-gpt"]
+    h, L = 256, 4
+    assert unique_params(w.model) == 1024 * h + 128 * h + L * (12 * h * h + 13 * h) + 2 * h
+    assert unique_params(w.model) == 3_454_464
+
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_unique_params_from_tensor_table(name):
+    m = MICRO_MODELS[name]
+    assert sum(t["rows"] * t["cols"] for t in oracle.tensors(m)) == unique_params(m)
+
+
+# ---------------------------------------------------------------- brute force
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_bruteforce_equals_lcm_items(name):
+    """Element-by-element enumeration equals the LCM workload-item form."""
+    m = MICRO_MODELS[name]
+    for a, b in cfg_pairs(m):
+        I = oracle.matrices(m, a, b)
+        B = oracle.matrices(m, a, b, brute=True)
+        for k in I:
+            np.testing.assert_array_equal(I[k], B[k], err_msg=f"{name} {a}->{b} {k}")
+
+
+def test_bruteforce_tiny():
+    w = WORKLOADS["tiny-gpt"]
+    I = oracle.matrices(w.model, w.src, w.dst)
+    B = oracle.matrices(w.model, w.src, w.dst, brute=True)
+    for k in I:
+        np.testing.assert_array_equal(I[k], B[k])
+
+
+# ---------------------------------------------------------------- invariants
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_identity_config_is_diagonal(name):
+    m = MICRO_MODELS[name]
+    for c in {a for a, _ in cfg_pairs(m)}:
+        M = oracle.matrices(m, c, c)
+        for k in ("route", "overlap_sharded"):
+            x = M[k]
+            assert (x == np.diag(np.diag(x))).all(), (name, c, k)
+        assert (np.diag(M["cost"]) == 0).all()
+        for d in range(c.world):
+            assert M["route"][d, d] == 14 * rank_elems(m, c, d)
+
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_overlap_sums(name):
+    """OVERLAP_SHARDED rows/columns sum to each rank's singly-held bytes;
+    OVERLAP sums count every copy of a replicated element."""
+    m = MICRO_MODELS[name]
+    T = oracle.tensors(m)
+    for a, b in cfg_pairs(m):
+        M = oracle.matrices(m, a, b)
+
+        def copies(cfg, t):
+            roles = 2 if (T[t]["tied_copy"] and cfg.pp > 1) else 1
+            return roles * (cfg.tp if T[t]["split"] == 0 else 1)
+
+        single = {t for t in range(len(T)) if copies(a, t) == 1 and copies(b, t) == 1}
+        for s in range(a.world):
+            pcs = oracle.layout(m, a, s)[0]
+            sh = sum((p["r1"] - p["r0"]) * (p["c1"] - p["c0"]) for p in pcs if p["tensor"] in single)
+            assert int(M["overlap_sharded"][s].sum()) == 14 * sh
+            ov = sum((p["r1"] - p["r0"]) * (p["c1"] - p["c0"]) * copies(b, p["tensor"]) for p in pcs)
+            assert int(M["overlap"][s].sum()) == 14 * ov
+        for d in range(b.world):
+            pcs = oracle.layout(m, b, d)[0]
+            sh = sum((p["r1"] - p["r0"]) * (p["c1"] - p["c0"]) for p in pcs if p["tensor"] in single)
+            assert int(M["overlap_sharded"][:, d].sum()) == 14 * sh
+        # COST = bytes(d) - OVERLAP (paper's c_ij, in bytes)
+        for d in range(b.world):
+            for s in range(a.world):
+                assert M["cost"][d, s] == 14 * rank_elems(m, b, d) - M["overlap"][s, d]
+
+
+def test_replicated_sender_round_robin():
+    """TP 2 -> 4 (PP 1): target d keeps what source d holds; targets 2, 3
+    take replicated tensors from source d mod 2."""
+    m = MICRO_MODELS["gpt"]
+    a, b = Parallel(2, 1), Parallel(4, 1)
+    T = oracle.tensors(m)
+    for d in range(4):
+        for s in range(2):
+            boxes, _ = oracle.message(m, a, b, s, d)
+            repl = {x["tensor"] for x in boxes if T[x["tensor"]]["split"] == 0}
+            all_repl = {i for i, t in enumerate(T) if t["split"] == 0}
+            if s == d % 2:
+                assert repl == all_repl
+            else:
+                assert repl == set()
+
+
+def test_meta_model_rule():
+    """Sec. III-D: the sliced dim is the one where full / local == TP; the
+    slice of one workload item is full / LCM(TP_prev, TP_curr)."""
+    for w in WORKLOADS.values():
+        T = oracle.tensors(w.model)
+        for cfg in (w.src, w.dst):
+            for p in oracle.layout(w.model, cfg, 0)[0]:
+                t = T[p["tensor"]]
+                ratios = (t["rows"] // (p["r1"] - p["r0"]), t["cols"] // (p["c1"] - p["c0"]))
+                if t["split"] == 0:
+                    assert ratios == (1, 1)
+                else:
+                    assert sorted(ratios) == [1, cfg.tp] or cfg.tp == 1
+                    assert ratios[t["split"] - 1] == cfg.tp
+        L = lcm(w.src.tp, w.dst.tp)
+        for d in range(w.dst.world):
+            for s in range(w.src.world):
+                for x in oracle.message(w.model, w.src, w.dst, s, d)[0][:8]:
+                    t = T[x["tensor"]]
+                    if t["split"] == 1:
+                        assert (x["r1"] - x["r0"]) % (t["rows"] // L) == 0
+                    elif t["split"] == 2:
+                        assert (x["c1"] - x["c0"]) % (t["cols"] // L) == 0
+            break
+
+
+def test_layout_structure():
+    """Pieces are disjoint, in order, start at multiples of 128 elements
+    except the up half of a fused gate/up pair, which follows gate."""
+    for w in list(WORKLOADS.values()) + []:
+        T = oracle.tensors(w.model)
+        for cfg in (w.src, w.dst):
+            for r in range(min(cfg.world, 4)):
+                pcs, elems = oracle.layout(w.model, cfg, r)
+                end = 0
+                for i, p in enumerate(pcs):
+                    n = (p["r1"] - p["r0"]) * (p["c1"] - p["c0"])
+                    if T[p["tensor"]]["fused_prev"]:
+                        assert p["off"] == end and pcs[i - 1]["tensor"] == p["tensor"] - 1
+                    else:
+                        assert p["off"] % 128 == 0 and p["off"] >= end
+                    end = p["off"] + n
+                assert elems >= end and elems % 128 == 0
+
+
+# ---------------------------------------------------------------- data movement
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_round_trip_identity(name):
+    """A -> B -> A leaves every source arena unchanged."""
+    m = MICRO_MODELS[name]
+    for a, b in cfg_pairs(m):
+        src = host_arenas(m, a, range(a.world), seed=7)
+        mid = empty_arenas(m, b, range(b.world))
+        oracle.migrate(m, a, b, src, mid)
+        back = empty_arenas(m, a, range(a.world))
+        oracle.migrate(m, b, a, mid, back)
+        for s in range(a.world):
+            for k in range(4):
+                assert np.array_equal(src[s][k], back[s][k]), (name, a, b, s, k)
+
+
+def test_round_trip_tiny():
+    w = WORKLOADS["tiny-gpt"]
+    src = host_arenas(w.model, w.src, range(w.src.world), w.seed)
+    mid = empty_arenas(w.model, w.dst, range(w.dst.world))
+    oracle.migrate(w.model, w.src, w.dst, src, mid)
+    back = empty_arenas(w.model, w.src, range(w.src.world))
+    oracle.migrate(w.model, w.dst, w.src, mid, back)
+    for s in range(w.src.world):
+        for k in range(4):
+            assert np.array_equal(src[s][k], back[s][k])
+
+
+def _check_seeded_values(model, cfg, arenas, seed):
+    T = oracle.tensors(model)
+    for r, ar in arenas.items():
+        for p in oracle.layout(model, cfg, r)[0]:
+            rows = np.arange(p["r0"], p["r1"], dtype=np.uint64)
+            cols = np.arange(p["c0"], p["c1"], dtype=np.uint64)
+            idx = (rows[:, None] * np.uint64(T[p["tensor"]]["cols"]) + cols[None, :]).ravel()
+            n = idx.size
+            for k in range(4):
+                want = synth.values(seed, k, p["tensor"], idx)
+                got = ar[k].view(want.dtype)[p["off"]:p["off"] + n]
+                assert np.array_equal(got, want), (r, p, k)
+
+
+def test_tiny_targets_hold_seeded_values():
+    """Every target element equals the seeded value of its logical index: a
+    pin independent of how the migration moves data."""
+    w = WORKLOADS["tiny-gpt"]
+    src = host_arenas(w.model, w.src, range(w.src.world), w.seed)
+    dst = empty_arenas(w.model, w.dst, range(w.dst.world))
+    oracle.migrate(w.model, w.src, w.dst, src, dst)
+    _check_seeded_values(w.model, w.dst, dst, w.seed)
+
+
+@pytest.mark.parametrize("name", ["ragged_llama", "llama_gqa", "gpt"])
+def test_micro_targets_hold_seeded_values(name):
+    m = MICRO_MODELS[name]
+    for a, b in cfg_pairs(m)[::3]:
+        src = host_arenas(m, a, range(a.world), 11)
+        dst = empty_arenas(m, b, range(b.world))
+        oracle.migrate(m, a, b, src, dst)
+        _check_seeded_values(m, b, dst, 11)
+
+
+def test_tp_change_equals_concatenation():
+    """PP 1, TP 2 -> 4: concatenating the targets' shards of each split tensor
+    along its split dim gives the same full tensor as concatenating the
+    sources' shards (numpy.concatenate as the library routine)."""
+    m = MICRO_MODELS["llama_gqa"]
+    a, b = Parallel(2, 1), Parallel(4, 1)
+    T = oracle.tensors(m)
+    src = host_arenas(m, a, range(2), 5)
+    dst = empty_arenas(m, b, range(4))
+    oracle.migrate(m, a, b, src, dst)
+
+    def full(cfg, arenas, t, k):
+        parts = []
+        for r in range(cfg.world):
+            for p in oracle.layout(m, cfg, r)[0]:
+                if p["tensor"] == t and p["role"] == 0:
+                    shp = (p["r1"] - p["r0"], p["c1"] - p["c0"])
+                    dt = np.uint16 if k == 0 else np.uint32
+                    x = arenas[r][k].view(dt)[p["off"]:p["off"] + shp[0] * shp[1]].reshape(shp)
+                    parts.append(x)
+        if T[t]["split"] == 0:
+            return parts[0]
+        return np.concatenate(parts, axis=T[t]["split"] - 1)
+
+    for t in range(len(T)):
+        for k in range(4):
+            np.testing.assert_array_equal(full(a, src, t, k), full(b, dst, t, k))
+
+
+def test_pp_change_is_block_copy():
+    """TP unchanged, PP 4 -> 2: a target's layer pieces are byte copies of the
+    matching source pieces (memcpy as the library routine)."""
+    m = MICRO_MODELS["llama_gqa"]
+    a, b = Parallel(2, 4), Parallel(2, 2)
+    src = host_arenas(m, a, range(a.world), 3)
+    dst = empty_arenas(m, b, range(b.world))
+    oracle.migrate(m, a, b, src, dst)
+    for d in range(b.world):
+        for q in oracle.layout(m, b, d)[0]:
+            n = (q["r1"] - q["r0"]) * (q["c1"] - q["c0"])
+            hit = 0
+            for s in range(a.world):
+                for p in oracle.layout(m, a, s)[0]:
+                    if (p["tensor"], p["r0"], p["r1"], p["c0"], p["c1"]) == (
+                            q["tensor"], q["r0"], q["r1"], q["c0"], q["c1"]):
+                        for k in range(4):
+                            e = ESIZE[k]
+                            assert bytes(dst[d][k][q["off"] * e:(q["off"] + n) * e]) == \
+                                bytes(src[s][k][p["off"] * e:(p["off"] + n) * e])
+                        hit += 1
+            assert hit >= 1
+
+
+# ---------------------------------------------------------------- wire format
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS) + ["tiny"])
+def test_messages_rebuild_targets(name):
+    """Placing every message box (row-major, full-tensor coordinates) into the
+    target arenas reproduces the materialize-then-cut result, and message
+    sizes are ROUTE rounded up to 8-element boxes."""
+    if name == "tiny":
+        w = WORKLOADS["tiny-gpt"]
+        m, pairs, seed = w.model, [(w.src, w.dst)], w.seed
+    else:
+        m, pairs, seed = MICRO_MODELS[name], cfg_pairs(MICRO_MODELS[name])[::4], 9
+    T = oracle.tensors(m)
+    for a, b in pairs:
+        src = host_arenas(m, a, range(a.world), seed)
+        dst = empty_arenas(m, b, range(b.world))
+        bufs = send_bufs(m, a, b, range(a.world))
+        oracle.migrate(m, a, b, src, dst, bufs)
+        rebuilt = empty_arenas(m, b, range(b.world))
+        R = oracle.matrices(m, a, b)["route"]
+        for s in range(a.world):
+            cnt, pad, dsp, tot = oracle.send_layout(m, a, b, s)
+            np.testing.assert_array_equal(cnt, R[s])
+            assert (dsp % 256 == 0).all() and tot == len(bufs[s])
+            for d in range(b.world):
+                boxes, npad = oracle.message(m, a, b, s, d)
+                assert pad[d] == 14 * npad
+                dpieces = oracle.layout(m, b, d)[0]
+                sec = 0
+                for k in range(4):
+                    e = ESIZE[k]
+                    base = int(dsp[d]) + sec
+                    for x in boxes:
+                        assert x["moff"] % 8 == 0
+                        h, wdt = x["r1"] - x["r0"], x["c1"] - x["c0"]
+                        blk = bufs[s][base + x["moff"] * e: base + (x["moff"] + h * wdt) * e]
+                        blk = blk.reshape(h, wdt * e)
+                        q = next(q for q in dpieces if q["tensor"] == x["tensor"] and q["role"] == x["role_d"])
+                        ld = q["c1"] - q["c0"]
+                        for i in range(h):
+                            o = q["off"] + (x["r0"] - q["r0"] + i) * ld + (x["c0"] - q["c0"])
+                            rebuilt[d][k][o * e:(o + wdt) * e] = blk[i]
+                        padn = (-(h * wdt)) % 8
+                        tail = bufs[s][base + (x["moff"] + h * wdt) * e: base + (x["moff"] + h * wdt + padn) * e]
+                        assert not tail.any()
+                    sec += npad * e
+        for d in range(b.world):
+            for k in range(4):
+                assert np.array_equal(rebuilt[d][k], dst[d][k]), (name, a, b, d, k)
+
+
+# ---------------------------------------------------------------- origins
+
+def test_origins_match_migration():
+    """Per-element origin queries (used for sampled checks at full size) agree
+    with the full migration on a micro model."""
+    m = MICRO_MODELS["ragged_gpt"]
+    a, b = Parallel(2, 2), Parallel(4, 1)
+    src = host_arenas(m, a, range(a.world), 2)
+    dst = empty_arenas(m, b, range(b.world))
+    bufs = send_bufs(m, a, b, range(a.world))
+    oracle.migrate(m, a, b, src, dst, bufs)
+    for d in range(b.world):
+        elems = oracle.layout(m, b, d)[1]
+        rk, so = oracle.dst_origin(m, a, b, d, np.arange(elems))
+        for k in range(4):
+            dt = np.uint16 if k == 0 else np.uint32
+            got = dst[d][k].view(dt)
+            for j in range(elems):
+                if rk[j] >= 0:
+                    assert got[j] == src[rk[j]][k].view(dt)[so[j]]
+    for s in range(a.world):
+        cnt, pad, dsp, tot = oracle.send_layout(m, a, b, s)
+        for d in range(b.world):
+            npad = int(pad[d]) // 14
+            so = oracle.msg_origin(m, a, b, s, d, np.arange(npad))
+            sec = int(dsp[d])
+            for k in range(4):
+                dt = np.uint16 if k == 0 else np.uint32
+                msg = bufs[s][sec:sec + npad * ESIZE[k]].view(dt)
+                for j in range(npad):
+                    want = 0 if so[j] == np.uint64(2**64 - 1) else src[s][k].view(dt)[so[j]]
+                    assert msg[j] == want
+                sec += npad * ESIZE[k]
+
+
+# ---------------------------------------------------------------- errors
+
+def test_error_codes():
+    m = MICRO_MODELS["gpt"]
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.matrices(m, Parallel(3, 1), Parallel(1, 1))
+    assert e.value.code == oracle.EINDIV
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.matrices(m, Parallel(1, 3), Parallel(1, 1))
+    assert e.value.code == oracle.EINDIV
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.matrices(m, Parallel(1, 1, 2), Parallel(1, 1))
+    assert e.value.code == oracle.EUNSUP
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.layout(m, Parallel(2, 1), 2)
+    assert e.value.code == oracle.ERANK
+
+
+def test_migrate_detects_disagreeing_replicas():
+    """A planted mismatch between two replicas is reported, not copied."""
+    m = MICRO_MODELS["gpt"]
+    a, b = Parallel(2, 1), Parallel(1, 1)
+    src = host_arenas(m, a, range(2), 1)
+    # flip one bit of ln1.weight on rank 1 (replicated across TP)
+    T = oracle.tensors(m)
+    t = next(i for i, x in enumerate(T) if x["name"].endswith("ln1.weight"))
+    p = next(p for p in oracle.layout(m, a, 1)[0] if p["tensor"] == t)
+    src[1][1][p["off"] * 4] ^= 1
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.migrate(m, a, b, src, empty_arenas(m, b, [0]))
+    assert e.value.code == oracle.EMISMATCH
+
+
+def test_migrate_detects_uncovered():
+    """A target element whose only holder is not resident is an error."""
+    m = MICRO_MODELS["gpt"]
+    a, b = Parallel(2, 1), Parallel(1, 1)
+    src = host_arenas(m, a, [0], 1)
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.migrate(m, a, b, src, empty_arenas(m, b, [0]))
+    assert e.value.code == oracle.EUNCOVERED
