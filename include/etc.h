@@ -1,0 +1,229 @@
+/*
+ * etc.h -- libetc: checkpoint-free resharding of GPU-resident model states
+ * between two hybrid-parallel (TP, PP) configurations, for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The operation (paper: "Direct Model State Migration for Elastic Training of
+ * Large Language Models", Sec. III):
+ *   - A rank's *workload* is the list of logical tensor pieces it holds under
+ *     Megatron's even static partition rules; every rank can derive every
+ *     other rank's workload locally (Sec. III-B).
+ *   - TP-split dims are compared at LCM(tp_prev, tp_curr) granularity
+ *     (Sec. III-C).
+ *   - The cost matrix counts, for every (new rank, old rank) pair, the data the
+ *     new rank lacks if it reuses the old one: c_ij = len(curr_i) -
+ *     len(curr_i intersect prev_j) (Sec. III-B).
+ *   - Pieces held by both sides of a pair stay (Refer); others are sent by
+ *     one holder and received by the new owner (Send / Recv, Sec. III-D).  The
+ *     states of every workload type move together: bf16 parameter, fp32
+ *     master, fp32 Adam m, fp32 Adam v (Sec. III-D).
+ * This library is the data-parallel hot path of that migration on one GPU:
+ *   etc_plan        host: layouts, routing, message layout, tile tables
+ *   etc_cost_matrix device: byte matrices over every (source, target) pair
+ *   etc_pack        device: a source rank's shards -> one message per peer
+ *   etc_unpack      device: received messages -> the target rank's shards
+ * Moving messages between GPUs is the caller's business (a grouped
+ * send/recv or all-to-all-v with the counts from etc_plan_send_layout).
+ *
+ * Conventions shared by all calls
+ *   Ranks.   rank = pp * TP + tp (TP fastest); data parallel must be 1.
+ *   Layers.  Stage p holds layers [p*L/PP, (p+1)*L/PP); the embedding (and a
+ *            GPT position table) sits on the first stage; the final norm and
+ *            the output head on the last.  A tied embedding also has a
+ *            duplicate on the last stage when PP > 1 ("copy role" 1).
+ *   TP split. Column-parallel weights and biases split dim 0 (QKV rows are
+ *            interleaved per KV group, so a shard is a contiguous row range),
+ *            row-parallel weights split dim 1, norms and row-parallel biases
+ *            are replicated, the vocab-parallel embedding and head split
+ *            dim 0.  SwiGLU gate and up are separate logical tensors stored
+ *            fused (gate shard, then up shard).
+ *   Arenas.  Each rank keeps one arena per state kind (kind 0 bf16 param,
+ *            1 fp32 master, 2 fp32 Adam m, 3 fp32 Adam v).  Local tensors
+ *            are laid out in tensor order (role-1 copies last), each starting
+ *            at a multiple of 128 elements (the up half of gate/up directly
+ *            after gate); element offsets are the same in all four arenas.
+ *            Bytes between tensors are never read or written.
+ *   Messages. Message s->d holds four kind sections (param, master, m, v),
+ *            each the routed boxes in d's arena order, every box row-major
+ *            in full-tensor coordinates and starting at a multiple of 8
+ *            elements (zero padded).  A send buffer holds the messages in
+ *            target order, each at a multiple of 256 bytes.
+ *   Memory.  The caller owns every arena, send buffer, message and output
+ *            buffer.  All device pointers must be 256-byte aligned.
+ *   Streams. Device calls only enqueue work on `stream` (a hipStream_t;
+ *            NULL is the null stream) and return; they never allocate,
+ *            free or synchronize.  Arguments are checked before anything is
+ *            enqueued; a non-zero status means nothing was enqueued.
+ *   Threads. A plan is immutable after etc_plan returns: any number of
+ *            threads may use it at once, on any streams of its device.
+ *   Errors.  Status 0 is success, negative values are ETC_ERR_*; the text
+ *            of the last error of the calling thread is etc_last_error().
+ */
+#ifndef ETC_H
+#define ETC_H
+
+#include <stdint.h>
+
+/* exported from libetc.so (the library is built with hidden visibility) */
+#define ETC_API __attribute__((visibility("default")))
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ETC_ARCH_GPT = 0,   /* LayerNorm w+b, linear biases, learned positions, GeLU MLP */
+       ETC_ARCH_LLAMA = 1  /* RMSNorm, no biases, SwiGLU gate/up + down, GQA            */ };
+
+enum { ETC_F_LAYERS_ONLY = 1 /* model flag: transformer layers only (no embeddings,
+                                final norm or head) */ };
+
+enum { ETC_KIND_PARAM_BF16 = 0, ETC_KIND_MASTER_F32 = 1, ETC_KIND_ADAM_M_F32 = 2,
+       ETC_KIND_ADAM_V_F32 = 3, ETC_NUM_KINDS = 4 };
+
+/* Matrix selectors for etc_cost_matrix (all values in bytes, over the four
+ * state kinds = 14 bytes per element):
+ *  ROUTE            S x D: bytes source s sends to target d.  Each target
+ *                   element is sent once.  Target d keeps what source rank d
+ *                   already holds (Refer).  Any other element comes from the
+ *                   holder with the smallest key (copy role differs,
+ *                   tp_s != tp_d mod TP_src, pp_s, tp_s).
+ *  OVERLAP          S x D: bytes of (held by s) intersect (needed by d), by
+ *                   logical identity (a replica counts as held).
+ *  OVERLAP_SHARDED  S x D: OVERLAP over tensors with exactly one copy in both
+ *                   configurations.
+ *  COST             D x S: the paper's cost matrix c_ij (rows are the new
+ *                   ranks, columns the old ranks, Sec. III-B):
+ *                   bytes(d) - OVERLAP[s][d]. */
+enum { ETC_CM_ROUTE = 0, ETC_CM_OVERLAP = 1, ETC_CM_OVERLAP_SHARDED = 2, ETC_CM_COST = 3 };
+
+enum { ETC_ALL_RANKS = -1 };
+
+enum { ETC_SIDE_SRC = 0, ETC_SIDE_DST = 1 };
+
+/* etc_plan flags */
+enum { ETC_PLAN_HOST_ONLY = 1 /* build host tables only: no device memory, no
+                                 device calls allowed on this plan */ };
+
+enum {
+  ETC_OK = 0,
+  ETC_ERR_INVALID_ARG = -1, /* NULL or out-of-range argument                      */
+  ETC_ERR_INDIVISIBLE = -2, /* a dim the configuration splits does not divide     */
+  ETC_ERR_RANK = -3,        /* rank out of range, or not built into this plan     */
+  ETC_ERR_ALIGN = -4,       /* a device pointer is not 256-byte aligned           */
+  ETC_ERR_UNSUPPORTED = -5, /* dp != 1, too many peers, or a size limit exceeded  */
+  ETC_ERR_NOMEM = -6,       /* host or device allocation failed (etc_plan only)   */
+  ETC_ERR_HIP = -7          /* a HIP runtime call failed; see etc_last_error()    */
+};
+
+typedef struct {
+  int32_t arch;            /* ETC_ARCH_*                                  */
+  int32_t num_layers;      /* transformer layers L                        */
+  int32_t hidden;          /* hidden size h                               */
+  int32_t num_heads;       /* attention (query) heads                     */
+  int32_t num_kv_heads;    /* KV heads (== num_heads without GQA)         */
+  int32_t ffn_hidden;      /* MLP inner size f                            */
+  int32_t vocab;           /* padded vocabulary size V                    */
+  int32_t max_pos;         /* learned position table rows (GPT), 0 = none */
+  int32_t tied_embeddings; /* 1: output head is the input embedding       */
+  int32_t flags;           /* ETC_F_*                                     */
+} etc_model_desc;
+
+typedef struct {
+  int32_t tp, pp, dp; /* dp must be 1 */
+} etc_parallel_cfg;
+
+typedef struct etc_plan_s etc_plan_t;
+
+/* One local piece of a logical tensor on a rank. */
+typedef struct {
+  char name[48];           /* e.g. "layers.3.qkv.weight"                  */
+  int32_t tensor;          /* logical tensor id (arena order)             */
+  int32_t role;            /* copy role: 0, or 1 for the tied duplicate   */
+  int64_t full_rows, full_cols; /* logical (TP = 1) shape; vectors [n, 1] */
+  int64_t r0, r1, c0, c1;  /* the piece's box in full-tensor coordinates  */
+  uint64_t elem_offset;    /* element offset in each of the four arenas;
+                              the piece is stored row-major, row length
+                              c1 - c0                                      */
+} etc_piece_info;
+
+/* Build a migration plan from `model`, the old configuration `src` and the new
+ * configuration `dst` (Sec. III: the primitive's inputs are the two parallel
+ * configurations and the model).  Host work: the logical tensor table, every
+ * rank's layout, the routing of every target element, every message layout.
+ * Device tables (routed boxes cut into uniform tiles, and the tensor table for
+ * etc_cost_matrix) are built for source rank `rank` and target rank `rank`
+ * (a process is both the old and the new owner of its GPU), or for all ranks
+ * with ETC_ALL_RANKS, and copied to the current device, which the plan is
+ * then bound to.  With ETC_PLAN_HOST_ONLY no device memory is touched.
+ * On success *out owns host and device memory until etc_plan_free.
+ * Errors: INVALID_ARG, INDIVISIBLE, UNSUPPORTED (dp != 1, GPT with GQA),
+ * RANK, NOMEM, HIP. */
+ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
+             const etc_parallel_cfg* dst, int rank, uint32_t flags, etc_plan_t** out);
+
+/* Release a plan (NULL is a no-op).  Device work using it must be complete. */
+ETC_API void etc_plan_free(etc_plan_t* plan);
+
+/* S = source world size, D = target world size. */
+ETC_API int etc_plan_dims(const etc_plan_t* plan, int* S, int* D);
+
+/* Number of logical tensors. */
+ETC_API int etc_plan_num_tensors(const etc_plan_t* plan, int* n);
+
+/* Arena length of a rank, in elements (multiply by 2 for kind 0, 4 for
+ * kinds 1..3 to get bytes).  side: ETC_SIDE_SRC or ETC_SIDE_DST. */
+ETC_API int etc_plan_arena_elems(const etc_plan_t* plan, int side, int rank, uint64_t* elems);
+
+/* Pieces of a rank, in arena order. */
+ETC_API int etc_plan_num_pieces(const etc_plan_t* plan, int side, int rank, int* n);
+ETC_API int etc_plan_piece(const etc_plan_t* plan, int side, int rank, int index, etc_piece_info* out);
+
+/* Send layout of source rank s (any rank, whatever the plan's `rank`):
+ * counts[d] = routed bytes to target d (= ROUTE[s][d]); msg_bytes[d] = bytes
+ * of message s->d including box padding (0 when nothing is routed);
+ * displs[d] = byte offset of message s->d in s's send buffer; *total = send
+ * buffer length.  Any output pointer may be NULL.  Arrays have D entries. */
+ETC_API int etc_plan_send_layout(const etc_plan_t* plan, int src_rank, uint64_t* counts,
+                         uint64_t* msg_bytes, uint64_t* displs, uint64_t* total);
+
+/* counts[s] = bytes target d receives from source s (= ROUTE[s][d]); S entries. */
+ETC_API int etc_plan_recv_counts(const etc_plan_t* plan, int dst_rank, uint64_t* counts);
+
+/* Compute one S x D (or D x S for ETC_CM_COST) uint64 matrix, row-major, into
+ * device memory d_out, with one GPU kernel over every (source, target) pair
+ * and every logical tensor (Sec. III-B, cost matrix; Sec. III-C, LCM items).
+ * d_out must be 8-byte aligned.
+ * Errors: INVALID_ARG (bad `which`, NULL, host-only plan), ALIGN, HIP. */
+ETC_API int etc_cost_matrix(const etc_plan_t* plan, int which, uint64_t* d_out, void* stream);
+
+/* Pack: copy source rank src_rank's shards (src_arena[k] = its arena of kind
+ * k, device memory, read only) into send_buf (device, etc_plan_send_layout
+ * total bytes): one contiguous message per target peer, the Send side of
+ * Sec. III-D.  Every message byte is written (box padding is zero); other
+ * bytes of send_buf are not touched.
+ * Errors: INVALID_ARG, RANK (src_rank not built into the plan), ALIGN, HIP. */
+ETC_API int etc_pack(const etc_plan_t* plan, int src_rank, const void* const src_arena[4],
+             void* send_buf, void* stream);
+
+/* Unpack: scatter the messages target dst_rank receives into its arenas
+ * (dst_arena[k], device memory), the Recv / Refer side of Sec. III-D.  msg[s]
+ * (S entries, device memory, read only) is the start of message s->dst_rank,
+ * laid out as etc_pack writes it; it may be NULL when ROUTE[s][dst_rank] is 0.
+ * Every payload element of the target arenas is written exactly once; bytes
+ * between tensors are not touched.
+ * Errors: INVALID_ARG (a needed msg[s] is NULL), RANK, ALIGN, UNSUPPORTED
+ * (more than ETC_MAX_PEERS sources feed this target), HIP. */
+ETC_API int etc_unpack(const etc_plan_t* plan, int dst_rank, const void* const* msg,
+               void* const dst_arena[4], void* stream);
+
+enum { ETC_MAX_PEERS = 128 };
+
+/* Text of the calling thread's last error ("" if none).  Valid until the
+ * thread's next failing call. */
+ETC_API const char* etc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ETC_H */

@@ -1,0 +1,305 @@
+// capi.hip -- the C ABI of libetc (include/etc.h): argument checks, error
+// reporting, device table upload and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <memory>
+#include <new>
+#include <string>
+
+#include "etc.h"
+#include "etc_internal.hpp"
+#include "plan.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(ETC_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+void release_device(etc_plan_t* P) {
+  if (P->device < 0) return;
+  int prev = -1;
+  const bool have_prev = hipGetDevice(&prev) == hipSuccess;
+  if (prev != P->device) (void)hipSetDevice(P->device);
+  if (P->d_boxes) (void)hipFree(P->d_boxes);
+  if (P->d_route_tensors) (void)hipFree(P->d_route_tensors);
+  if (have_prev && prev != P->device) (void)hipSetDevice(prev);
+  P->d_boxes = nullptr;
+  P->d_route_tensors = nullptr;
+}
+
+int check_device_plan(const etc_plan_t* P) {
+  if (!P) return fail(ETC_ERR_INVALID_ARG, "plan is NULL");
+  if (P->device < 0 || !P->d_route_tensors)
+    return fail(ETC_ERR_INVALID_ARG, "plan was built with ETC_PLAN_HOST_ONLY");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != P->device)
+    return fail(ETC_ERR_INVALID_ARG, "current device " + std::to_string(dev) +
+                                         " is not the plan's device " + std::to_string(P->device));
+  return ETC_OK;
+}
+
+int upload(etc_plan_t* P, int rank) {
+  using namespace etc;
+  const int S = P->src.world(), D = P->dst.world();
+  hipError_t e = hipGetDevice(&P->device);
+  if (e != hipSuccess) {
+    P->device = -1;
+    return hip_fail(e, "hipGetDevice");
+  }
+  int ncu = 0;
+  e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, P->device);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  // several resident workgroups per CU keep enough 16-byte loads in flight
+  P->copy_grid = uint32_t(std::max(1, ncu) * 8);
+
+  std::vector<CopyBox> all;
+  for (int s = 0; s < S; ++s) {
+    if (rank != ETC_ALL_RANKS && rank != s) continue;
+    CopyTable& t = P->pack_tab[s];
+    auto v = build_pack_boxes(*P, s, &t.bytes);
+    t.first = uint32_t(all.size());
+    t.nbox = uint32_t(v.size() - 1);
+    t.ntiles = v.back().tile0;
+    t.built = true;
+    all.insert(all.end(), v.begin(), v.end());
+  }
+  for (int d = 0; d < D; ++d) {
+    if (rank != ETC_ALL_RANKS && rank != d) continue;
+    CopyTable& t = P->unpack_tab[d];
+    auto v = build_unpack_boxes(*P, d, &t.peers, &t.bytes);
+    t.first = uint32_t(all.size());
+    t.nbox = uint32_t(v.size() - 1);
+    t.ntiles = v.back().tile0;
+    t.built = true;
+    all.insert(all.end(), v.begin(), v.end());
+  }
+  if (!all.empty()) {
+    e = hipMalloc(&P->d_boxes, all.size() * sizeof(CopyBox));
+    if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    e = hipMemcpy(P->d_boxes, all.data(), all.size() * sizeof(CopyBox), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy (copy tables)");
+  }
+  const size_t rt_bytes = std::max<size_t>(1, P->route_tensors.size()) * sizeof(RouteTensor);
+  e = hipMalloc(&P->d_route_tensors, rt_bytes);
+  if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+  if (!P->route_tensors.empty()) {
+    e = hipMemcpy(P->d_route_tensors, P->route_tensors.data(),
+                  P->route_tensors.size() * sizeof(RouteTensor), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy (tensor table)");
+  }
+  return ETC_OK;
+}
+
+int check_side_rank(const etc_plan_t* P, int side, int rank) {
+  if (!P) return fail(ETC_ERR_INVALID_ARG, "plan is NULL");
+  if (side != ETC_SIDE_SRC && side != ETC_SIDE_DST) return fail(ETC_ERR_INVALID_ARG, "bad side");
+  const int n = side == ETC_SIDE_SRC ? P->src.world() : P->dst.world();
+  if (rank < 0 || rank >= n) return fail(ETC_ERR_RANK, "rank " + std::to_string(rank) + " out of range");
+  return ETC_OK;
+}
+
+int check_arenas(const void* const* arenas, const char* what) {
+  if (!arenas) return fail(ETC_ERR_INVALID_ARG, std::string(what) + " is NULL");
+  for (int k = 0; k < 4; ++k) {
+    if (!arenas[k]) return fail(ETC_ERR_INVALID_ARG, std::string(what) + "[" + std::to_string(k) + "] is NULL");
+    if (!aligned(arenas[k], 256))
+      return fail(ETC_ERR_ALIGN, std::string(what) + "[" + std::to_string(k) + "] is not 256-byte aligned");
+  }
+  return ETC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
+             int rank, uint32_t flags, etc_plan_t** out) {
+  if (!out) return fail(ETC_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!model || !src || !dst) return fail(ETC_ERR_INVALID_ARG, "model, src and dst must not be NULL");
+  if (flags & ~uint32_t(ETC_PLAN_HOST_ONLY)) return fail(ETC_ERR_INVALID_ARG, "unknown plan flags");
+  std::unique_ptr<etc_plan_t> P;
+  try {
+    etc::validate(*model, *src, *dst);
+    P.reset(new etc_plan_t());
+    P->model = *model;
+    P->src = etc::Grid{src->tp, src->pp};
+    P->dst = etc::Grid{dst->tp, dst->pp};
+    P->rank = rank;
+    P->flags = flags;
+    const int S = P->src.world(), D = P->dst.world();
+    if (rank != ETC_ALL_RANKS && (rank < 0 || rank >= std::max(S, D)))
+      return fail(ETC_ERR_RANK, "rank " + std::to_string(rank) + " is neither a source nor a target rank");
+    etc::build_host_plan(*P);
+    P->pack_tab.resize(S);
+    P->unpack_tab.resize(D);
+    if (!(flags & ETC_PLAN_HOST_ONLY)) {
+      const int rc = upload(P.get(), rank);
+      if (rc != ETC_OK) {
+        release_device(P.get());
+        return rc;
+      }
+    }
+  } catch (const etc::PlanError& e) {
+    if (P) release_device(P.get());
+    return fail(e.code, e.what());
+  } catch (const std::bad_alloc&) {
+    if (P) release_device(P.get());
+    return fail(ETC_ERR_NOMEM, "host allocation failed");
+  }
+  *out = P.release();
+  g_last_error.clear();
+  return ETC_OK;
+}
+
+void etc_plan_free(etc_plan_t* plan) {
+  if (!plan) return;
+  release_device(plan);
+  delete plan;
+}
+
+int etc_plan_dims(const etc_plan_t* P, int* S, int* D) {
+  if (!P) return fail(ETC_ERR_INVALID_ARG, "plan is NULL");
+  if (S) *S = P->src.world();
+  if (D) *D = P->dst.world();
+  return ETC_OK;
+}
+
+int etc_plan_num_tensors(const etc_plan_t* P, int* n) {
+  if (!P || !n) return fail(ETC_ERR_INVALID_ARG, "NULL argument");
+  *n = int(P->tensors.size());
+  return ETC_OK;
+}
+
+int etc_plan_arena_elems(const etc_plan_t* P, int side, int rank, uint64_t* elems) {
+  int rc = check_side_rank(P, side, rank);
+  if (rc) return rc;
+  if (!elems) return fail(ETC_ERR_INVALID_ARG, "elems is NULL");
+  *elems = (side == ETC_SIDE_SRC ? P->src_layout : P->dst_layout)[rank].elems;
+  return ETC_OK;
+}
+
+int etc_plan_num_pieces(const etc_plan_t* P, int side, int rank, int* n) {
+  int rc = check_side_rank(P, side, rank);
+  if (rc) return rc;
+  if (!n) return fail(ETC_ERR_INVALID_ARG, "n is NULL");
+  *n = int((side == ETC_SIDE_SRC ? P->src_layout : P->dst_layout)[rank].pieces.size());
+  return ETC_OK;
+}
+
+int etc_plan_piece(const etc_plan_t* P, int side, int rank, int index, etc_piece_info* out) {
+  int rc = check_side_rank(P, side, rank);
+  if (rc) return rc;
+  const auto& L = (side == ETC_SIDE_SRC ? P->src_layout : P->dst_layout)[rank];
+  if (!out || index < 0 || index >= int(L.pieces.size()))
+    return fail(ETC_ERR_INVALID_ARG, "bad piece index");
+  const etc::Piece& p = L.pieces[index];
+  const etc::LogicalTensor& t = P->tensors[p.tensor];
+  std::memset(out, 0, sizeof *out);
+  std::strncpy(out->name, t.name.c_str(), sizeof(out->name) - 1);
+  out->tensor = p.tensor;
+  out->role = p.role;
+  out->full_rows = t.rows;
+  out->full_cols = t.cols;
+  out->r0 = p.r0;
+  out->r1 = p.r1;
+  out->c0 = p.c0;
+  out->c1 = p.c1;
+  out->elem_offset = p.off;
+  return ETC_OK;
+}
+
+int etc_plan_send_layout(const etc_plan_t* P, int s, uint64_t* counts, uint64_t* msg_bytes,
+                         uint64_t* displs, uint64_t* total) {
+  int rc = check_side_rank(P, ETC_SIDE_SRC, s);
+  if (rc) return rc;
+  const int D = P->dst.world();
+  for (int d = 0; d < D; ++d) {
+    const size_t sd = size_t(s) * D + d;
+    if (counts) counts[d] = P->msg_elems[sd] * 14;
+    if (msg_bytes) msg_bytes[d] = P->msg_npad[sd] * 14;
+    if (displs) displs[d] = P->msg_displ[sd];
+  }
+  if (total) *total = P->sendbuf_bytes[s];
+  return ETC_OK;
+}
+
+int etc_plan_recv_counts(const etc_plan_t* P, int d, uint64_t* counts) {
+  int rc = check_side_rank(P, ETC_SIDE_DST, d);
+  if (rc) return rc;
+  if (!counts) return fail(ETC_ERR_INVALID_ARG, "counts is NULL");
+  const int S = P->src.world(), D = P->dst.world();
+  for (int s = 0; s < S; ++s) counts[s] = P->msg_elems[size_t(s) * D + d] * 14;
+  return ETC_OK;
+}
+
+int etc_cost_matrix(const etc_plan_t* P, int which, uint64_t* d_out, void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (which < ETC_CM_ROUTE || which > ETC_CM_COST) return fail(ETC_ERR_INVALID_ARG, "bad matrix selector");
+  if (!d_out) return fail(ETC_ERR_INVALID_ARG, "d_out is NULL");
+  if (!aligned(d_out, 8)) return fail(ETC_ERR_ALIGN, "d_out is not 8-byte aligned");
+  hipError_t e = etc::launch_cost(P->d_route_tensors, int(P->route_tensors.size()), P->src.world(),
+                                  P->dst.world(), P->src.tp, P->dst.tp, which, d_out,
+                                  static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "cost matrix launch");
+  return ETC_OK;
+}
+
+int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* send_buf, void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (s < 0 || s >= P->src.world()) return fail(ETC_ERR_RANK, "source rank out of range");
+  const etc::CopyTable& t = P->pack_tab[s];
+  if (!t.built) return fail(ETC_ERR_RANK, "source rank " + std::to_string(s) + " is not built into this plan");
+  if ((rc = check_arenas(src_arena, "src_arena"))) return rc;
+  if (!send_buf) return fail(ETC_ERR_INVALID_ARG, "send_buf is NULL");
+  if (!aligned(send_buf, 256)) return fail(ETC_ERR_ALIGN, "send_buf is not 256-byte aligned");
+  void* arenas[4];
+  for (int k = 0; k < 4; ++k) arenas[k] = const_cast<void*>(src_arena[k]);
+  void* peers[1] = {send_buf};
+  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid, arenas,
+                                  peers, 1, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pack launch");
+  return ETC_OK;
+}
+
+int etc_unpack(const etc_plan_t* P, int d, const void* const* msg, void* const dst_arena[4], void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
+  const etc::CopyTable& t = P->unpack_tab[d];
+  if (!t.built) return fail(ETC_ERR_RANK, "target rank " + std::to_string(d) + " is not built into this plan");
+  if ((rc = check_arenas(const_cast<const void* const*>(dst_arena), "dst_arena"))) return rc;
+  if (!msg && !t.peers.empty()) return fail(ETC_ERR_INVALID_ARG, "msg is NULL");
+  void* peers[ETC_MAX_PEERS];
+  for (size_t i = 0; i < t.peers.size(); ++i) {
+    const void* p = msg[t.peers[i]];
+    if (!p) return fail(ETC_ERR_INVALID_ARG, "msg[" + std::to_string(t.peers[i]) + "] is NULL but source " +
+                                                 std::to_string(t.peers[i]) + " sends to this target");
+    if (!aligned(p, 256)) return fail(ETC_ERR_ALIGN, "msg[" + std::to_string(t.peers[i]) + "] is not 256-byte aligned");
+    peers[i] = const_cast<void*>(p);
+  }
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
+                                  dst_arena, peers, int(t.peers.size()), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "unpack launch");
+  return ETC_OK;
+}
+
+const char* etc_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,170 @@
+// copy.hip -- the pack / unpack copy engine for gfx950 (MI355X).
+//
+// Pure data movement, HBM bound: each launch copies a list of routed boxes
+// between a rank's four state arenas (strided rows) and message sections
+// (contiguous rows), for all four state kinds.  Boxes are pre-cut on the host
+// into uniform tiles of about kTileElems elements per kind; the grid is a
+// few workgroups per CU, and each workgroup walks one contiguous range of
+// tiles.  A tile's descriptor is uniform across the workgroup (read once per
+// box through the scalar cache).  Within a tile, the 256 threads move 16-byte
+// vectors, several loads in flight per thread before the matching stores;
+// stores and loads are non-temporal because nothing is reused.
+#include <hip/hip_runtime.h>
+
+#include "copy_geom.hpp"
+#include "etc_internal.hpp"
+
+namespace etc {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct CopyArgs {
+  const CopyBox* boxes;  // nbox boxes + 1 sentinel (tile0 = ntiles)
+  uint32_t nbox;
+  uint32_t ntiles;
+  char* arena[4];
+  char* peer[ETC_MAX_PEERS];
+};
+
+constexpr int kUnroll = 4;
+
+// Copy nr rows of row_bytes bytes (16-byte aligned starts, row_bytes a
+// multiple of 16 when nr > 1) from src (row pitch sld bytes) to dst (pitch dld).
+__device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64_t sld,
+                                            char* __restrict__ dst, uint64_t dld, uint32_t nr,
+                                            uint32_t row_bytes) {
+  const uint32_t vpr = row_bytes >> 4;
+  const uint32_t nv = nr * vpr;
+  uint32_t i = threadIdx.x;
+  if (nr == 1) {
+    for (; i + (kUnroll - 1) * kCopyThreads < nv; i += kUnroll * kCopyThreads) {
+      u32x4 v[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+        v[u] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(src + uint64_t(i + u * kCopyThreads) * 16));
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+        __builtin_nontemporal_store(
+            v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
+    }
+    for (; i < nv; i += kCopyThreads)
+      __builtin_nontemporal_store(
+          __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + uint64_t(i) * 16)),
+          reinterpret_cast<u32x4*>(dst + uint64_t(i) * 16));
+    return;
+  }
+  for (; i + (kUnroll - 1) * kCopyThreads < nv; i += kUnroll * kCopyThreads) {
+    u32x4 v[kUnroll];
+    uint32_t r[kUnroll], c[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t idx = i + u * kCopyThreads;
+      r[u] = idx / vpr;
+      c[u] = idx - r[u] * vpr;
+      v[u] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4*>(src + r[u] * sld + uint64_t(c[u]) * 16));
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      __builtin_nontemporal_store(v[u],
+                                  reinterpret_cast<u32x4*>(dst + r[u] * dld + uint64_t(c[u]) * 16));
+  }
+  for (; i < nv; i += kCopyThreads) {
+    const uint32_t r = i / vpr, c = i - r * vpr;
+    __builtin_nontemporal_store(
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + r * sld + uint64_t(c) * 16)),
+        reinterpret_cast<u32x4*>(dst + r * dld + uint64_t(c) * 16));
+  }
+}
+
+// Element-wise copy of columns [c_begin, nc) of nr rows (any alignment).
+template <typename E>
+__device__ __forceinline__ void copy_elems_2d(const E* __restrict__ src, uint64_t sld,
+                                              E* __restrict__ dst, uint64_t dld, uint32_t nr,
+                                              uint32_t c_begin, uint32_t nc) {
+  const uint32_t w = nc - c_begin;
+  const uint32_t n = nr * w;
+  for (uint32_t i = threadIdx.x; i < n; i += kCopyThreads) {
+    const uint32_t r = i / w, c = c_begin + (i - r * w);
+    dst[r * dld + c] = src[r * sld + c];
+  }
+}
+
+template <bool kPack, int kKind>
+__device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox& b, char* mbase,
+                                               const TileGeom& g) {
+  constexpr int es = kKind == 0 ? 2 : 4;
+  using E = typename std::conditional<es == 2, uint16_t, uint32_t>::type;
+  char* A = a.arena[kKind] + tile_arena_elem(b, g) * es;
+  char* Mb = mbase + section_byte(b.msg_npad, kKind);  // this kind's section of the message
+  char* M = Mb + tile_msg_elem(b, g) * es;
+  const char* src = kPack ? A : M;
+  char* dst = kPack ? M : A;
+  const uint64_t sld = uint64_t(kPack ? b.a_ld : b.cols) * es;
+  const uint64_t dld = uint64_t(kPack ? b.cols : b.a_ld) * es;
+  const bool vec = (b.vec >> (es == 2 ? 0 : 1)) & 1;
+  if (vec) {
+    constexpr uint32_t vw = 16 / es;
+    const uint32_t nvc = g.nr == 1 ? (g.nc / vw) * vw : g.nc;  // vector part of each row
+    copy_vec_2d(src, sld, dst, dld, g.nr, nvc * es);
+    if (nvc < g.nc)
+      copy_elems_2d<E>(reinterpret_cast<const E*>(src), sld / es, reinterpret_cast<E*>(dst),
+                       dld / es, g.nr, nvc, g.nc);
+  } else {
+    copy_elems_2d<E>(reinterpret_cast<const E*>(src), sld / es, reinterpret_cast<E*>(dst),
+                     dld / es, g.nr, 0, g.nc);
+  }
+  if (kPack && g.last && b.pad) {
+    // zero the padding that rounds the box up to a multiple of 8 elements
+    E* tail = reinterpret_cast<E*>(Mb + (b.m_off + uint64_t(b.rows) * b.cols) * es);
+    if (threadIdx.x < b.pad) tail[threadIdx.x] = 0;
+  }
+}
+
+template <bool kPack>
+__global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
+  uint32_t t0, t1;
+  block_tiles(blockIdx.x, gridDim.x, a.ntiles, &t0, &t1);
+  if (t0 >= t1) return;
+  uint32_t bi = box_of_tile(a.boxes, a.nbox, t0);
+  CopyBox b = a.boxes[bi];
+  uint32_t next0 = a.boxes[bi + 1].tile0;
+  for (uint32_t t = t0; t < t1; ++t) {
+    while (t >= next0) {
+      ++bi;
+      b = a.boxes[bi];
+      next0 = a.boxes[bi + 1].tile0;
+    }
+    const TileGeom g = tile_geom(b, t, next0);
+    char* mbase = a.peer[b.peer] + b.msg_byte;
+    copy_tile_kind<kPack, 0>(a, b, mbase, g);
+    copy_tile_kind<kPack, 1>(a, b, mbase, g);
+    copy_tile_kind<kPack, 2>(a, b, mbase, g);
+    copy_tile_kind<kPack, 3>(a, b, mbase, g);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
+                       uint32_t grid, void* const arena[4], void* const* peers, int npeers,
+                       hipStream_t stream) {
+  if (ntiles == 0) return hipSuccess;
+  CopyArgs a{};
+  a.boxes = boxes;
+  a.nbox = nbox;
+  a.ntiles = ntiles;
+  for (int k = 0; k < 4; ++k) a.arena[k] = static_cast<char*>(arena[k]);
+  for (int p = 0; p < npeers; ++p) a.peer[p] = static_cast<char*>(peers[p]);
+  const uint32_t g = grid < ntiles ? grid : ntiles;
+  if (pack)
+    hipLaunchKernelGGL(copy_kernel<true>, dim3(g), dim3(kCopyThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(copy_kernel<false>, dim3(g), dim3(kCopyThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace etc

@@ -1,0 +1,64 @@
+// copy_geom.hpp -- tile geometry of the copy engine: which tiles a workgroup
+// owns, which box a tile belongs to, and the rows and columns of a tile.
+// Host and device share it, so the planner's bounds checks and the kernel
+// walk the same tiles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "etc_internal.hpp"
+
+namespace etc {
+
+// Contiguous tile range [t0, t1) of workgroup `bid` out of G.
+__host__ __device__ inline void block_tiles(uint32_t bid, uint32_t G, uint32_t ntiles,
+                                            uint32_t* t0, uint32_t* t1) {
+  *t0 = uint32_t(uint64_t(bid) * ntiles / G);
+  *t1 = uint32_t(uint64_t(bid + 1) * ntiles / G);
+}
+
+// Index of the box holding tile t: the last box with tile0 <= t.
+__host__ __device__ inline uint32_t box_of_tile(const CopyBox* boxes, uint32_t nbox, uint32_t t) {
+  uint32_t lo = 0, hi = nbox;
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (boxes[mid].tile0 <= t) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+struct TileGeom {
+  uint32_t r0, c0, nr, nc;  // tile rows [r0, r0+nr), columns [c0, c0+nc) of the box
+  bool last;                // last tile of its box
+};
+
+// Geometry of tile t of box b (next0 = first tile of the next box).
+__host__ __device__ inline TileGeom tile_geom(const CopyBox& b, uint32_t t, uint32_t next0) {
+  TileGeom g;
+  const uint32_t j = t - b.tile0;
+  const uint32_t band = j / b.ntc, tcol = j - band * b.ntc;
+  g.r0 = band * b.tr;
+  g.c0 = tcol * b.tc;
+  g.nr = b.tr < b.rows - g.r0 ? b.tr : b.rows - g.r0;
+  g.nc = b.tc < b.cols - g.c0 ? b.tc : b.cols - g.c0;
+  g.last = t + 1 == next0;
+  return g;
+}
+
+// Element offsets of a tile's first element on each side.
+__host__ __device__ inline uint64_t tile_arena_elem(const CopyBox& b, const TileGeom& g) {
+  return b.a_off + uint64_t(g.r0) * b.a_ld + g.c0;
+}
+__host__ __device__ inline uint64_t tile_msg_elem(const CopyBox& b, const TileGeom& g) {
+  return b.m_off + uint64_t(g.r0) * b.cols + g.c0;
+}
+
+// Byte offset of kind k's section inside a message of npad elements per section.
+__host__ __device__ inline uint64_t section_byte(uint64_t npad, int k) {
+  return npad * (k == 0 ? 0 : (k == 1 ? 2 : (k == 2 ? 6 : 10)));
+}
+
+}  // namespace etc

@@ -1,0 +1,136 @@
+// etc_internal.hpp -- internal types of libetc (host planner + gfx950 kernels).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "etc.h"
+
+namespace etc {
+
+// ---------------------------------------------------------------------------
+// Logical tensors and rank layouts (host)
+// ---------------------------------------------------------------------------
+
+enum Split : int32_t { kRepl = 0, kRows = 1, kCols = 2 };
+enum Home : int32_t { kFirstStage = 0, kOwnLayer = 1, kLastStage = 2 };
+
+struct LogicalTensor {
+  std::string name;
+  int64_t rows = 0, cols = 0;  // full (TP = 1) shape; vectors are [n, 1]
+  Split split = kRepl;
+  Home home = kOwnLayer;
+  int32_t layer = -1;
+  bool tied_dup = false;  // duplicate (copy role 1) on the last stage when PP > 1
+  bool fused = false;     // stored right after the previous tensor (up after gate)
+};
+
+struct Grid {
+  int tp = 1, pp = 1;
+  int world() const { return tp * pp; }
+};
+
+struct Piece {
+  int32_t tensor, role;
+  int64_t r0, r1, c0, c1;  // full-tensor box
+  uint64_t off;            // arena element offset
+  int64_t ld() const { return c1 - c0; }
+  uint64_t elems() const { return uint64_t((r1 - r0) * (c1 - c0)); }
+};
+
+struct RankLayout {
+  std::vector<Piece> pieces;
+  std::vector<int32_t> piece_of_tensor[2];  // [role][tensor] -> piece index or -1
+  uint64_t elems = 0;
+};
+
+// ---------------------------------------------------------------------------
+// Per-tensor routing record, shared by the host planner and the cost kernel
+// ---------------------------------------------------------------------------
+
+struct RouteTensor {
+  int64_t rows, cols;
+  int32_t split;         // Split
+  int32_t src_stage[2];  // stage holding copy role 0 / 1 in the source grid, -1 none
+  int32_t dst_stage[2];  // same in the target grid
+  int32_t single_copy;   // exactly one copy in both grids
+};
+
+// ---------------------------------------------------------------------------
+// Copy engine descriptors (device)
+// ---------------------------------------------------------------------------
+
+// One routed box between an arena (strided rows) and a message section
+// (contiguous, row-major).  Element offsets are kind-independent; the kernel
+// scales them by each kind's element size.  64 bytes.
+struct CopyBox {
+  uint64_t a_off;     // arena element offset of the box's first element
+  uint64_t m_off;     // element offset inside each kind section of the message
+  uint64_t msg_byte;  // byte offset of the message from its peer base pointer
+  uint64_t msg_npad;  // elements per kind section of that message
+  uint32_t a_ld;      // arena row stride, elements
+  uint32_t rows, cols;  // box shape; contiguous boxes are collapsed to one row
+  uint32_t tr, tc;    // tile shape (rows x cols)
+  uint32_t ntc;       // tiles per row band
+  uint32_t tile0;     // first tile of this box in its launch
+  uint16_t peer;      // peer slot
+  uint8_t pad;        // zero elements after the box in the message (pack)
+  uint8_t vec;        // bit0: 16-byte vectors valid for 2-byte kinds, bit1: for 4-byte kinds
+};
+static_assert(sizeof(CopyBox) == 64, "CopyBox layout");
+
+// Launch table of one rank's pack or unpack.
+struct CopyTable {
+  bool built = false;
+  uint32_t first = 0;   // index of the first box in the plan's device box array
+  uint32_t nbox = 0;    // boxes (the array holds one more sentinel box)
+  uint32_t ntiles = 0;
+  uint64_t bytes = 0;   // payload bytes moved (all four kinds)
+  std::vector<int32_t> peers;  // unpack: source rank of each peer slot
+};
+
+constexpr uint32_t kTileElems = 16384;  // nominal tile: 16384 elements per kind
+constexpr int kCopyThreads = 256;
+constexpr int kCmThreads = 256;
+
+// kernel launchers (copy.hip, cost.hip)
+hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
+                       uint32_t grid, void* const arena[4], void* const* peers, int npeers,
+                       hipStream_t stream);
+hipError_t launch_cost(const RouteTensor* rt, int nt, int S, int D, int tps, int tpd, int which,
+                       uint64_t* out, hipStream_t stream);
+
+}  // namespace etc
+
+// The opaque plan.
+struct etc_plan_s {
+  etc_model_desc model{};
+  etc::Grid src, dst;
+  int rank = ETC_ALL_RANKS;
+  uint32_t flags = 0;
+  std::vector<etc::LogicalTensor> tensors;
+  std::vector<etc::RouteTensor> route_tensors;
+  std::vector<etc::RankLayout> src_layout, dst_layout;
+
+  // messages, indexed [s * D + d]
+  struct MsgBox {
+    int32_t tensor, role_d;
+    int64_t r0, r1, c0, c1;
+    uint64_t moff;
+  };
+  std::vector<std::vector<MsgBox>> msg;
+  std::vector<uint64_t> msg_elems;  // routed elements
+  std::vector<uint64_t> msg_npad;   // padded elements per kind section
+  std::vector<uint64_t> msg_displ;  // byte displacement in the sender's buffer
+  std::vector<uint64_t> sendbuf_bytes;
+
+  // device side
+  int device = -1;
+  uint32_t copy_grid = 0;
+  etc::RouteTensor* d_route_tensors = nullptr;
+  etc::CopyBox* d_boxes = nullptr;
+  std::vector<etc::CopyTable> pack_tab, unpack_tab;
+};

@@ -1,0 +1,380 @@
+// plan.hip -- host planner: tensor table, rank layouts, routing, message
+// layouts and the tiled copy tables uploaded for the gfx950 kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+#include <stdexcept>
+#include <string>
+
+#include "etc_internal.hpp"
+#include "plan.hpp"
+#include "route.hpp"
+
+namespace etc {
+
+namespace {
+
+int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// A layer tensor of an architecture: name, shape, how TP splits it.
+struct LayerSpec {
+  const char* name;
+  int64_t rows, cols;
+  Split split;
+  bool fused;
+};
+
+std::vector<LayerSpec> layer_specs(const etc_model_desc& m) {
+  const int64_t h = m.hidden, f = m.ffn_hidden;
+  if (m.arch == ETC_ARCH_GPT) {
+    // Megatron GPT block: column-parallel QKV and FC1 (weights and biases),
+    // row-parallel projection and FC2 (their biases and the norms replicated).
+    return {{"ln1.weight", h, 1, kRepl, false},  {"ln1.bias", h, 1, kRepl, false},
+            {"qkv.weight", 3 * h, h, kRows, false}, {"qkv.bias", 3 * h, 1, kRows, false},
+            {"proj.weight", h, h, kCols, false}, {"proj.bias", h, 1, kRepl, false},
+            {"ln2.weight", h, 1, kRepl, false},  {"ln2.bias", h, 1, kRepl, false},
+            {"fc1.weight", f, h, kRows, false},  {"fc1.bias", f, 1, kRows, false},
+            {"fc2.weight", h, f, kCols, false},  {"fc2.bias", h, 1, kRepl, false}};
+  }
+  // Llama block: RMSNorms replicated; QKV rows grouped per KV head group;
+  // SwiGLU gate and up column-parallel and stored fused; down row-parallel.
+  const int64_t head_dim = h / m.num_heads;
+  const int64_t qkv_rows = int64_t(m.num_heads + 2 * m.num_kv_heads) * head_dim;
+  return {{"norm1.weight", h, 1, kRepl, false}, {"qkv.weight", qkv_rows, h, kRows, false},
+          {"proj.weight", h, h, kCols, false},  {"norm2.weight", h, 1, kRepl, false},
+          {"gate.weight", f, h, kRows, false},  {"up.weight", f, h, kRows, true},
+          {"down.weight", h, f, kCols, false}};
+}
+
+}  // namespace
+
+std::vector<LogicalTensor> build_tensor_table(const etc_model_desc& m) {
+  std::vector<LogicalTensor> out;
+  const bool whole_model = !(m.flags & ETC_F_LAYERS_ONLY);
+  auto push = [&](std::string name, int64_t r, int64_t c, Split sp, Home home, int layer,
+                  bool tied, bool fused) {
+    LogicalTensor t;
+    t.name = std::move(name);
+    t.rows = r;
+    t.cols = c;
+    t.split = sp;
+    t.home = home;
+    t.layer = layer;
+    t.tied_dup = tied;
+    t.fused = fused;
+    out.push_back(std::move(t));
+  };
+  const int64_t h = m.hidden, V = m.vocab;
+  if (whole_model) {
+    push("embed", V, h, kRows, kFirstStage, -1, m.tied_embeddings != 0, false);
+    if (m.arch == ETC_ARCH_GPT && m.max_pos > 0)
+      push("pos_embed", m.max_pos, h, kRepl, kFirstStage, -1, false, false);
+  }
+  const auto specs = layer_specs(m);
+  for (int l = 0; l < m.num_layers; ++l)
+    for (const auto& s : specs)
+      push("layers." + std::to_string(l) + "." + s.name, s.rows, s.cols, s.split, kOwnLayer, l,
+           false, s.fused);
+  if (whole_model) {
+    if (m.arch == ETC_ARCH_GPT) {
+      push("final_ln.weight", h, 1, kRepl, kLastStage, -1, false, false);
+      push("final_ln.bias", h, 1, kRepl, kLastStage, -1, false, false);
+    } else {
+      push("final_norm.weight", h, 1, kRepl, kLastStage, -1, false, false);
+    }
+    if (!m.tied_embeddings) push("output.weight", V, h, kRows, kLastStage, -1, false, false);
+  }
+  return out;
+}
+
+int stage_of(const LogicalTensor& t, int role, const Grid& g, int num_layers) {
+  switch (t.home) {
+    case kOwnLayer:
+      return role == 0 ? t.layer / (num_layers / g.pp) : -1;
+    case kFirstStage:
+      if (role == 0) return 0;
+      return (t.tied_dup && g.pp > 1) ? g.pp - 1 : -1;
+    case kLastStage:
+      return role == 0 ? g.pp - 1 : -1;
+  }
+  return -1;
+}
+
+RankLayout build_layout(const std::vector<LogicalTensor>& T, const Grid& g, int num_layers,
+                        int rank) {
+  RankLayout L;
+  const int pp = rank / g.tp, tp = rank % g.tp;
+  const int nt = int(T.size());
+  L.piece_of_tensor[0].assign(nt, -1);
+  L.piece_of_tensor[1].assign(nt, -1);
+  uint64_t end = 0;
+  int last_tensor = -1, last_role = -1;
+  for (int role = 0; role < 2; ++role) {
+    for (int i = 0; i < nt; ++i) {
+      const LogicalTensor& t = T[i];
+      if (stage_of(t, role, g, num_layers) != pp) continue;
+      Piece p{};
+      p.tensor = i;
+      p.role = role;
+      p.r0 = 0;
+      p.r1 = t.rows;
+      p.c0 = 0;
+      p.c1 = t.cols;
+      if (t.split == kRows) {
+        p.r0 = tp * (t.rows / g.tp);
+        p.r1 = p.r0 + t.rows / g.tp;
+      } else if (t.split == kCols) {
+        p.c0 = tp * (t.cols / g.tp);
+        p.c1 = p.c0 + t.cols / g.tp;
+      }
+      const bool follows = t.fused && last_tensor == i - 1 && last_role == role;
+      p.off = follows ? end : uint64_t(round_up(int64_t(end), 128));
+      end = p.off + p.elems();
+      L.piece_of_tensor[role][i] = int32_t(L.pieces.size());
+      L.pieces.push_back(p);
+      last_tensor = i;
+      last_role = role;
+    }
+  }
+  L.elems = uint64_t(round_up(int64_t(end), 128));
+  return L;
+}
+
+// ---------------------------------------------------------------------------
+
+namespace {
+
+void fail(int code, const std::string& msg) { throw PlanError(code, msg); }
+
+void check_inputs(const etc_model_desc& m, const Grid& g, const char* which, int dp) {
+  if (dp != 1) fail(ETC_ERR_UNSUPPORTED, std::string(which) + ": data parallel size must be 1");
+  if (g.tp < 1 || g.pp < 1) fail(ETC_ERR_INVALID_ARG, std::string(which) + ": tp and pp must be >= 1");
+  auto need = [&](bool ok, const std::string& what) {
+    if (!ok)
+      fail(ETC_ERR_INDIVISIBLE, std::string(which) + " (tp=" + std::to_string(g.tp) + ", pp=" +
+                                    std::to_string(g.pp) + "): " + what);
+  };
+  need(m.num_layers % g.pp == 0, "num_layers must divide by pp");
+  need(m.hidden % g.tp == 0, "hidden must divide by tp");
+  need(m.ffn_hidden % g.tp == 0, "ffn_hidden must divide by tp");
+  need(m.num_kv_heads % g.tp == 0, "num_kv_heads must divide by tp (whole KV groups per shard)");
+  if (!(m.flags & ETC_F_LAYERS_ONLY)) need(m.vocab % g.tp == 0, "vocab must divide by tp");
+}
+
+void check_model(const etc_model_desc& m) {
+  if (m.arch != ETC_ARCH_GPT && m.arch != ETC_ARCH_LLAMA) fail(ETC_ERR_INVALID_ARG, "unknown arch");
+  if (m.num_layers < 1 || m.hidden < 1 || m.num_heads < 1 || m.num_kv_heads < 1 ||
+      m.ffn_hidden < 1)
+    fail(ETC_ERR_INVALID_ARG, "model sizes must be positive");
+  if (!(m.flags & ETC_F_LAYERS_ONLY) && m.vocab < 1) fail(ETC_ERR_INVALID_ARG, "vocab must be positive");
+  if (m.max_pos < 0) fail(ETC_ERR_INVALID_ARG, "max_pos must be >= 0");
+  if (m.hidden % m.num_heads || m.num_heads % m.num_kv_heads)
+    fail(ETC_ERR_INVALID_ARG, "hidden must divide by num_heads and num_heads by num_kv_heads");
+  if (m.arch == ETC_ARCH_GPT && m.num_kv_heads != m.num_heads)
+    fail(ETC_ERR_UNSUPPORTED, "GPT blocks have no grouped-query attention");
+  if (m.flags & ~uint32_t(ETC_F_LAYERS_ONLY)) fail(ETC_ERR_INVALID_ARG, "unknown model flags");
+}
+
+// Cut one routed box into tiles and fill its copy descriptor.
+CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint64_t m_off,
+                 uint64_t msg_byte, uint64_t msg_npad, int peer, bool pack, uint32_t tile0) {
+  CopyBox b{};
+  // a box whose rows are adjacent in the arena is one contiguous run
+  if (rows == 1 || cols == a_ld) {
+    cols = rows * cols;
+    rows = 1;
+    a_ld = cols;
+  }
+  if (cols > int64_t(UINT32_MAX) || rows > int64_t(UINT32_MAX) || a_ld > int64_t(UINT32_MAX))
+    fail(ETC_ERR_UNSUPPORTED, "a routed box exceeds 2^32 elements per row");
+  b.a_off = a_off;
+  b.m_off = m_off;
+  b.msg_byte = msg_byte;
+  b.msg_npad = msg_npad;
+  b.a_ld = uint32_t(a_ld);
+  b.rows = uint32_t(rows);
+  b.cols = uint32_t(cols);
+  if (cols >= int64_t(kTileElems)) {
+    b.tc = kTileElems;
+    b.tr = 1;
+  } else {
+    b.tc = uint32_t(cols);
+    b.tr = uint32_t(std::max<int64_t>(1, std::min<int64_t>(rows, kTileElems / cols)));
+  }
+  b.ntc = uint32_t((cols + b.tc - 1) / b.tc);
+  b.tile0 = tile0;
+  b.peer = uint16_t(peer);
+  const uint64_t n = uint64_t(rows) * uint64_t(cols);
+  b.pad = pack ? uint8_t((8 - n % 8) % 8) : 0;
+  // 16-byte vectors: 8 elements of a 2-byte kind, 4 of a 4-byte kind.  The
+  // message side starts every box at a multiple of 8 elements.
+  auto ok = [&](uint64_t w) {
+    if (a_off % w) return false;
+    if (rows > 1 && (uint64_t(a_ld) % w || uint64_t(cols) % w)) return false;
+    return true;
+  };
+  b.vec = uint8_t((ok(8) ? 1 : 0) | (ok(4) ? 2 : 0));
+  return b;
+}
+
+uint32_t box_tiles(const CopyBox& b) {
+  const uint64_t ntr = (uint64_t(b.rows) + b.tr - 1) / b.tr;
+  return uint32_t(ntr * b.ntc);
+}
+
+}  // namespace
+
+PlanError::PlanError(int c, std::string m) : std::runtime_error(std::move(m)), code(c) {}
+
+void build_host_plan(etc_plan_t& P) {
+  const etc_model_desc& m = P.model;
+  P.tensors = build_tensor_table(m);
+  const int nt = int(P.tensors.size());
+  const int S = P.src.world(), D = P.dst.world();
+  P.src_layout.resize(S);
+  P.dst_layout.resize(D);
+  for (int s = 0; s < S; ++s) P.src_layout[s] = build_layout(P.tensors, P.src, m.num_layers, s);
+  for (int d = 0; d < D; ++d) P.dst_layout[d] = build_layout(P.tensors, P.dst, m.num_layers, d);
+
+  P.route_tensors.resize(nt);
+  for (int i = 0; i < nt; ++i) {
+    const LogicalTensor& t = P.tensors[i];
+    RouteTensor& r = P.route_tensors[i];
+    r.rows = t.rows;
+    r.cols = t.cols;
+    r.split = t.split;
+    int copies_src = 0, copies_dst = 0;
+    for (int role = 0; role < 2; ++role) {
+      r.src_stage[role] = stage_of(t, role, P.src, m.num_layers);
+      r.dst_stage[role] = stage_of(t, role, P.dst, m.num_layers);
+      copies_src += r.src_stage[role] >= 0;
+      copies_dst += r.dst_stage[role] >= 0;
+    }
+    if (t.split == kRepl) {
+      copies_src *= P.src.tp;
+      copies_dst *= P.dst.tp;
+    }
+    r.single_copy = copies_src == 1 && copies_dst == 1;
+  }
+
+  // Route every target piece: per target rank, per piece in arena order, the
+  // sources that send part of it.  Messages list boxes in that order.
+  P.msg.assign(size_t(S) * D, {});
+  P.msg_elems.assign(size_t(S) * D, 0);
+  P.msg_npad.assign(size_t(S) * D, 0);
+  for (int d = 0; d < D; ++d) {
+    for (const Piece& q : P.dst_layout[d].pieces) {
+      const RouteTensor& rt = P.route_tensors[q.tensor];
+      uint64_t got = 0;
+      for (int s = 0; s < S; ++s) {
+        const Span x = routed_span(rt, s, d, S, P.src.tp, P.dst.tp);
+        if (x.len() == 0) continue;
+        etc_plan_s::MsgBox b{};
+        b.tensor = q.tensor;
+        b.role_d = q.role;
+        b.r0 = 0;
+        b.r1 = rt.rows;
+        b.c0 = 0;
+        b.c1 = rt.cols;
+        if (rt.split == kRows) {
+          b.r0 = x.lo;
+          b.r1 = x.hi;
+        } else if (rt.split == kCols) {
+          b.c0 = x.lo;
+          b.c1 = x.hi;
+        }
+        const uint64_t n = uint64_t((b.r1 - b.r0) * (b.c1 - b.c0));
+        const size_t sd = size_t(s) * D + d;
+        b.moff = P.msg_npad[sd];
+        P.msg_npad[sd] += uint64_t(round_up(int64_t(n), 8));
+        P.msg_elems[sd] += n;
+        P.msg[sd].push_back(b);
+        got += n;
+      }
+      if (got != q.elems())
+        fail(ETC_ERR_INVALID_ARG, "internal: target piece not covered exactly once");
+    }
+  }
+  P.msg_displ.assign(size_t(S) * D, 0);
+  P.sendbuf_bytes.assign(S, 0);
+  for (int s = 0; s < S; ++s) {
+    uint64_t cur = 0;
+    for (int d = 0; d < D; ++d) {
+      cur = uint64_t(round_up(int64_t(cur), 256));
+      P.msg_displ[size_t(s) * D + d] = cur;
+      cur += P.msg_npad[size_t(s) * D + d] * 14;
+    }
+    P.sendbuf_bytes[s] = uint64_t(round_up(int64_t(cur), 256));
+  }
+}
+
+std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, uint64_t* bytes) {
+  const int D = P.dst.world();
+  std::vector<CopyBox> v;
+  uint32_t tiles = 0;
+  uint64_t moved = 0;
+  const RankLayout& L = P.src_layout[s];
+  for (int d = 0; d < D; ++d) {
+    const size_t sd = size_t(s) * D + d;
+    for (const auto& b : P.msg[sd]) {
+      const int role_s = role_on(P.route_tensors[b.tensor].src_stage, s / P.src.tp);
+      const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
+      const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
+      CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_displ[sd],
+                           P.msg_npad[sd], 0, true, tiles);
+      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
+      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
+      tiles = uint32_t(nt);
+      moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
+      v.push_back(c);
+    }
+  }
+  CopyBox sentinel{};
+  sentinel.tile0 = tiles;
+  v.push_back(sentinel);
+  if (bytes) *bytes = moved;
+  return v;
+}
+
+std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,
+                                        uint64_t* bytes) {
+  const int S = P.src.world(), D = P.dst.world();
+  std::vector<CopyBox> v;
+  uint32_t tiles = 0;
+  uint64_t moved = 0;
+  const RankLayout& L = P.dst_layout[d];
+  peers->clear();
+  for (int s = 0; s < S; ++s) {
+    const size_t sd = size_t(s) * D + d;
+    if (P.msg[sd].empty()) continue;
+    const int slot = int(peers->size());
+    if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "more than ETC_MAX_PEERS sources feed one target");
+    peers->push_back(s);
+    for (const auto& b : P.msg[sd]) {
+      const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
+      const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
+      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, 0, P.msg_npad[sd],
+                           slot, false, tiles);
+      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
+      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
+      tiles = uint32_t(nt);
+      moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
+      v.push_back(c);
+    }
+  }
+  CopyBox sentinel{};
+  sentinel.tile0 = tiles;
+  v.push_back(sentinel);
+  if (bytes) *bytes = moved;
+  return v;
+}
+
+void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst) {
+  check_model(m);
+  check_inputs(m, Grid{src.tp, src.pp}, "source config", src.dp);
+  check_inputs(m, Grid{dst.tp, dst.pp}, "target config", dst.dp);
+}
+
+}  // namespace etc

@@ -1,0 +1,30 @@
+// plan.hpp -- host planner entry points (plan.hip).
+#pragma once
+
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "etc_internal.hpp"
+
+namespace etc {
+
+struct PlanError : std::runtime_error {
+  PlanError(int c, std::string m);
+  int code;
+};
+
+std::vector<LogicalTensor> build_tensor_table(const etc_model_desc& m);
+int stage_of(const LogicalTensor& t, int role, const Grid& g, int num_layers);
+RankLayout build_layout(const std::vector<LogicalTensor>& T, const Grid& g, int num_layers, int rank);
+
+// throws PlanError on bad input
+void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst);
+// layouts, routing, message layouts (host only)
+void build_host_plan(etc_plan_t& P);
+// copy descriptors of one rank (terminated by a sentinel box holding the tile count)
+std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, uint64_t* bytes);
+std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,
+                                        uint64_t* bytes);
+
+}  // namespace etc

@@ -1,0 +1,213 @@
+"""Python binding of libetc (include/etc.h): argument marshalling only.
+
+Every step of the resharding path runs in libetc.so -- the host planner and
+the gfx950 kernels.  There is no fallback: if the library is missing this
+module raises on import.  Device buffers are passed as torch tensors (or raw
+integer device pointers); torch only provides memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libetc.so")
+
+ARCH_GPT, ARCH_LLAMA = 0, 1
+F_LAYERS_ONLY = 1
+CM_ROUTE, CM_OVERLAP, CM_OVERLAP_SHARDED, CM_COST = 0, 1, 2, 3
+ALL_RANKS = -1
+SIDE_SRC, SIDE_DST = 0, 1
+PLAN_HOST_ONLY = 1
+OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP = \
+    0, -1, -2, -3, -4, -5, -6, -7
+MAX_PEERS = 128
+ESIZE = (2, 4, 4, 4)
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "arch", "num_layers", "hidden", "num_heads", "num_kv_heads", "ffn_hidden", "vocab",
+        "max_pos", "tied_embeddings", "flags")]
+
+
+class ParallelCfg(ctypes.Structure):
+    _fields_ = [("tp", ctypes.c_int32), ("pp", ctypes.c_int32), ("dp", ctypes.c_int32)]
+
+
+class PieceInfo(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("tensor", ctypes.c_int32), ("role", ctypes.c_int32),
+                ("full_rows", ctypes.c_int64), ("full_cols", ctypes.c_int64),
+                ("r0", ctypes.c_int64), ("r1", ctypes.c_int64), ("c0", ctypes.c_int64),
+                ("c1", ctypes.c_int64), ("elem_offset", ctypes.c_uint64)]
+
+
+class EtcError(RuntimeError):
+    def __init__(self, code, func, msg):
+        super().__init__(f"{func} failed ({code}): {msg}")
+        self.code = code
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libetc.so not found at {LIB_PATH}; build it with "
+                          "`python -m paper_2607_04749_amd.build` (no fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32p, u64p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_uint64)
+    L.etc_plan.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(ParallelCfg),
+                           ctypes.POINTER(ParallelCfg), ctypes.c_int, ctypes.c_uint32,
+                           ctypes.POINTER(vp)]
+    L.etc_plan_free.argtypes = [vp]
+    L.etc_plan_free.restype = None
+    L.etc_plan_dims.argtypes = [vp, i32p, i32p]
+    L.etc_plan_num_tensors.argtypes = [vp, i32p]
+    L.etc_plan_arena_elems.argtypes = [vp, ctypes.c_int, ctypes.c_int, u64p]
+    L.etc_plan_num_pieces.argtypes = [vp, ctypes.c_int, ctypes.c_int, i32p]
+    L.etc_plan_piece.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                 ctypes.POINTER(PieceInfo)]
+    L.etc_plan_send_layout.argtypes = [vp, ctypes.c_int, vp, vp, vp, u64p]
+    L.etc_plan_recv_counts.argtypes = [vp, ctypes.c_int, vp]
+    L.etc_cost_matrix.argtypes = [vp, ctypes.c_int, vp, vp]
+    L.etc_pack.argtypes = [vp, ctypes.c_int, vp, vp, vp]
+    L.etc_unpack.argtypes = [vp, ctypes.c_int, vp, vp, vp]
+    L.etc_last_error.argtypes = []
+    L.etc_last_error.restype = ctypes.c_char_p
+    return L
+
+
+_lib = _load()
+
+
+def lib():
+    return _lib
+
+
+def _check(rc, func):
+    if rc != OK:
+        raise EtcError(rc, func, _lib.etc_last_error().decode())
+
+
+def _ptr(x):
+    """Device pointer of a tensor, or an integer pointer, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Plan:
+    """Owns an etc_plan_t handle."""
+
+    def __init__(self, handle, model, src, dst, rank):
+        self._h = handle
+        self.model, self.src, self.dst, self.rank = model, src, dst, rank
+        S, D = ctypes.c_int(), ctypes.c_int()
+        _check(_lib.etc_plan_dims(handle, ctypes.byref(S), ctypes.byref(D)), "etc_plan_dims")
+        self.S, self.D = S.value, D.value
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise ValueError("plan was freed")
+        return self._h
+
+    def free(self):
+        if self._h:
+            _lib.etc_plan_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+    def num_tensors(self):
+        n = ctypes.c_int()
+        _check(_lib.etc_plan_num_tensors(self.handle, ctypes.byref(n)), "etc_plan_num_tensors")
+        return n.value
+
+    def arena_elems(self, side, rank):
+        e = ctypes.c_uint64()
+        _check(_lib.etc_plan_arena_elems(self.handle, side, rank, ctypes.byref(e)),
+               "etc_plan_arena_elems")
+        return e.value
+
+    def arena_bytes(self, side, rank):
+        e = self.arena_elems(side, rank)
+        return [e * s for s in ESIZE]
+
+    def pieces(self, side, rank):
+        n = ctypes.c_int()
+        _check(_lib.etc_plan_num_pieces(self.handle, side, rank, ctypes.byref(n)),
+               "etc_plan_num_pieces")
+        out = []
+        info = PieceInfo()
+        for i in range(n.value):
+            _check(_lib.etc_plan_piece(self.handle, side, rank, i, ctypes.byref(info)),
+                   "etc_plan_piece")
+            out.append(dict(name=info.name.decode(), tensor=info.tensor, role=info.role,
+                            full_rows=info.full_rows, full_cols=info.full_cols, r0=info.r0,
+                            r1=info.r1, c0=info.c0, c1=info.c1, off=info.elem_offset))
+        return out
+
+    def send_layout(self, s):
+        """(counts, msg_bytes, displs, total) for source rank s."""
+        cnt = np.zeros(self.D, np.uint64)
+        mb = np.zeros(self.D, np.uint64)
+        dsp = np.zeros(self.D, np.uint64)
+        tot = ctypes.c_uint64()
+        _check(_lib.etc_plan_send_layout(self.handle, s, cnt.ctypes.data, mb.ctypes.data,
+                                         dsp.ctypes.data, ctypes.byref(tot)),
+               "etc_plan_send_layout")
+        return cnt, mb, dsp, tot.value
+
+    def recv_counts(self, d):
+        cnt = np.zeros(self.S, np.uint64)
+        _check(_lib.etc_plan_recv_counts(self.handle, d, cnt.ctypes.data), "etc_plan_recv_counts")
+        return cnt
+
+
+def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0):
+    """model: object with astuple() (arch, layers, hidden, heads, kv_heads, ffn,
+    vocab, max_pos, tied, flags); src/dst: objects with astuple() (tp, pp, dp)."""
+    m = ModelDesc(*model.astuple())
+    a = ParallelCfg(*src.astuple())
+    b = ParallelCfg(*dst.astuple())
+    h = ctypes.c_void_p()
+    _check(_lib.etc_plan(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), rank, flags,
+                         ctypes.byref(h)), "etc_plan")
+    return Plan(h, model, src, dst, rank)
+
+
+def etc_cost_matrix(plan, which, out, stream=None):
+    """out: device buffer of S*D (D*S for CM_COST) uint64 (an int64 tensor works)."""
+    _check(_lib.etc_cost_matrix(plan.handle, which, _ptr(out), _stream(stream)), "etc_cost_matrix")
+
+
+def etc_pack(plan, src_rank, src_arenas, send_buf, stream=None):
+    arr = (ctypes.c_void_p * 4)(*[_ptr(x) for x in src_arenas])
+    _check(_lib.etc_pack(plan.handle, src_rank, ctypes.cast(arr, ctypes.c_void_p), _ptr(send_buf),
+                         _stream(stream)), "etc_pack")
+
+
+def etc_unpack(plan, dst_rank, msgs, dst_arenas, stream=None):
+    """msgs: S entries (tensor, int pointer or None)."""
+    if len(msgs) != plan.S:
+        raise ValueError(f"need {plan.S} message pointers, got {len(msgs)}")
+    m = (ctypes.c_void_p * plan.S)(*[_ptr(x) for x in msgs])
+    arr = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
+    _check(_lib.etc_unpack(plan.handle, dst_rank, ctypes.cast(m, ctypes.c_void_p),
+                           ctypes.cast(arr, ctypes.c_void_p), _stream(stream)), "etc_unpack")

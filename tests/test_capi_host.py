@@ -1,0 +1,127 @@
+"""Host side of libetc, no GPU: the library loads and exports every symbol
+the header declares; the planner's layouts, message layouts and routing agree
+with the oracle (they share no code); bad inputs give the documented errors."""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from micro import MICRO_MODELS, cfg_pairs
+from paper_2607_04749_amd import etc
+from paper_2607_04749_amd.workloads import GPT, LLAMA, WORKLOADS, ModelShape, Parallel
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HOST = etc.PLAN_HOST_ONLY
+
+
+def test_exports_match_header():
+    hdr = open(os.path.join(ROOT, "include", "etc.h")).read()
+    declared = set(re.findall(r"^ETC_API [^(]*?\b(etc_\w+)\(", hdr, flags=re.M))
+    assert {"etc_plan", "etc_cost_matrix", "etc_pack", "etc_unpack"} <= declared
+    out = subprocess.run(["nm", "-D", "--defined-only", etc.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    assert declared <= exported, declared - exported
+    for name in declared:
+        assert hasattr(etc.lib(), name)
+
+
+def _compare(model, a, b):
+    p = etc.etc_plan(model, a, b, flags=HOST)
+    assert (p.S, p.D) == (a.world, b.world)
+    assert p.num_tensors() == len(oracle.tensors(model))
+    for side, cfg in ((etc.SIDE_SRC, a), (etc.SIDE_DST, b)):
+        for r in range(cfg.world):
+            want, elems = oracle.layout(model, cfg, r)
+            got = p.pieces(side, r)
+            assert p.arena_elems(side, r) == elems
+            assert [(x["tensor"], x["role"], x["r0"], x["r1"], x["c0"], x["c1"], x["off"]) for x in got] == \
+                   [(x["tensor"], x["role"], x["r0"], x["r1"], x["c0"], x["c1"], x["off"]) for x in want]
+    R = oracle.matrices(model, a, b)["route"]
+    for s in range(a.world):
+        cnt, mb, dsp, tot = p.send_layout(s)
+        ocnt, opad, odsp, otot = oracle.send_layout(model, a, b, s)
+        np.testing.assert_array_equal(cnt, ocnt)
+        np.testing.assert_array_equal(mb, opad)
+        np.testing.assert_array_equal(dsp, odsp)
+        assert tot == otot
+    for d in range(b.world):
+        np.testing.assert_array_equal(p.recv_counts(d), R[:, d])
+    p.free()
+
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_planner_matches_oracle_micro(name):
+    m = MICRO_MODELS[name]
+    for a, b in cfg_pairs(m):
+        _compare(m, a, b)
+
+
+@pytest.mark.parametrize("wl", sorted(WORKLOADS))
+def test_planner_matches_oracle_workloads(wl):
+    w = WORKLOADS[wl]
+    _compare(w.model, w.src, w.dst)
+
+
+def test_piece_names_and_shapes():
+    w = WORKLOADS["llama-70b"]
+    p = etc.etc_plan(w.model, w.src, w.dst, rank=0, flags=HOST)
+    T = oracle.tensors(w.model)
+    for x in p.pieces(etc.SIDE_DST, 0):
+        t = T[x["tensor"]]
+        assert x["name"] == t["name"]
+        assert (x["full_rows"], x["full_cols"]) == (t["rows"], t["cols"])
+    qkv = [x for x in p.pieces(etc.SIDE_SRC, 0) if x["name"].endswith("qkv.weight")][0]
+    assert (qkv["r1"] - qkv["r0"], qkv["c1"] - qkv["c0"]) == (1280, 8192)
+
+
+@pytest.mark.parametrize("model,src,dst,code", [
+    (MICRO_MODELS["gpt"], Parallel(3, 1), Parallel(1, 1), etc.ERR_INDIVISIBLE),
+    (MICRO_MODELS["gpt"], Parallel(1, 3), Parallel(1, 1), etc.ERR_INDIVISIBLE),
+    (MICRO_MODELS["gpt"], Parallel(1, 1), Parallel(8, 1), etc.ERR_INDIVISIBLE),
+    (MICRO_MODELS["gpt"], Parallel(1, 1, 2), Parallel(1, 1), etc.ERR_UNSUPPORTED),
+    (MICRO_MODELS["gpt"], Parallel(0, 1), Parallel(1, 1), etc.ERR_INVALID_ARG),
+    (ModelShape(GPT, 4, 16, 4, 2, 32, 16, 8, 1), Parallel(1, 1), Parallel(1, 1), etc.ERR_UNSUPPORTED),
+    (ModelShape(LLAMA, 4, 16, 4, 3, 32, 16, 0, 0), Parallel(1, 1), Parallel(1, 1), etc.ERR_INVALID_ARG),
+    (ModelShape(7, 4, 16, 4, 4, 32, 16, 0, 0), Parallel(1, 1), Parallel(1, 1), etc.ERR_INVALID_ARG),
+])
+def test_plan_errors(model, src, dst, code):
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan(model, src, dst, flags=HOST)
+    assert e.value.code == code
+    assert etc.lib().etc_last_error()
+
+
+def test_rank_and_flag_errors():
+    w = WORKLOADS["tiny-gpt"]
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan(w.model, w.src, w.dst, rank=4, flags=HOST)
+    assert e.value.code == etc.ERR_RANK
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan(w.model, w.src, w.dst, flags=8)
+    assert e.value.code == etc.ERR_INVALID_ARG
+    p = etc.etc_plan(w.model, w.src, w.dst, flags=HOST)
+    with pytest.raises(etc.EtcError) as e:
+        p.pieces(etc.SIDE_SRC, 9)
+    assert e.value.code == etc.ERR_RANK
+    with pytest.raises(etc.EtcError) as e:
+        p.send_layout(-1)
+    assert e.value.code == etc.ERR_RANK
+    # device calls on a host-only plan are rejected before any device work
+    for call in (lambda: etc.etc_pack(p, 0, [0, 0, 0, 0], 0, stream=0),
+                 lambda: etc.etc_unpack(p, 0, [None] * 4, [0, 0, 0, 0], stream=0),
+                 lambda: etc.etc_cost_matrix(p, etc.CM_ROUTE, 0, stream=0)):
+        with pytest.raises(etc.EtcError) as e:
+            call()
+        assert e.value.code == etc.ERR_INVALID_ARG
+
+
+def test_rank_plan_send_layout_any_source():
+    """A plan built for one rank still reports every source's send layout."""
+    w = WORKLOADS["llama-13b"]
+    p = etc.etc_plan(w.model, w.src, w.dst, rank=0, flags=HOST)
+    for s in range(w.src.world):
+        np.testing.assert_array_equal(p.send_layout(s)[0], oracle.send_layout(w.model, w.src, w.dst, s)[0])
