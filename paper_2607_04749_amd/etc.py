@@ -11,6 +11,9 @@ import ctypes
 import os
 
 import numpy as np
+# torch first: it loads its HIP runtime, and libetc.so (NEEDED libamdhip64.so.7)
+# then binds to that same runtime instead of mapping a second one.
+import torch  # noqa: F401
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libetc.so")
@@ -50,6 +53,15 @@ class EtcError(RuntimeError):
         self.code = code
 
 
+def hip_runtimes():
+    """Distinct HIP runtime libraries mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({l.split()[-1] for l in f if "libamdhip64" in l})
+    except OSError:
+        return []
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"libetc.so not found at {LIB_PATH}; build it with "
@@ -74,6 +86,9 @@ def _load():
     L.etc_unpack.argtypes = [vp, ctypes.c_int, vp, vp, vp]
     L.etc_last_error.argtypes = []
     L.etc_last_error.restype = ctypes.c_char_p
+    if len(hip_runtimes()) > 1:
+        raise ImportError(f"two HIP runtimes are mapped ({hip_runtimes()}); import torch before "
+                          "loading libetc.so")
     return L
 
 

@@ -9,6 +9,7 @@ import os
 import subprocess
 
 import numpy as np
+import torch  # noqa: F401  (load torch's HIP runtime first; libsynth binds to it)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsynth.so")
