@@ -63,8 +63,15 @@ int upload(etc_plan_t* P, int rank) {
   int ncu = 0;
   e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, P->device);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  // several resident workgroups per CU keep enough 16-byte loads in flight
-  P->copy_grid = uint32_t(std::max(1, ncu) * 8);
+  // copy engine launch shape: one resident workgroup per CU, enforced by
+  // reserving just over half of the CU's LDS per workgroup
+  int lds_cu = 0, lds_block = 0;
+  e = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, P->device);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  e = hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, P->device);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  P->copy_grid = uint32_t(std::max(1, ncu));
+  P->copy_lds_reserve = uint32_t(std::max(0, std::min(lds_block, lds_cu / 2 + 256)));
 
   std::vector<CopyBox> all;
   for (int s = 0; s < S; ++s) {
@@ -272,8 +279,9 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
   void* arenas[4];
   for (int k = 0; k < 4; ++k) arenas[k] = const_cast<void*>(src_arena[k]);
   void* peers[1] = {send_buf};
-  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid, arenas,
-                                  peers, 1, static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
+                                  P->copy_lds_reserve, arenas, peers, 1,
+                                  static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
   return ETC_OK;
 }
@@ -295,7 +303,8 @@ int etc_unpack(const etc_plan_t* P, int d, const void* const* msg, void* const d
     peers[i] = const_cast<void*>(p);
   }
   hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  dst_arena, peers, int(t.peers.size()), static_cast<hipStream_t>(stream));
+                                  P->copy_lds_reserve, dst_arena, peers, int(t.peers.size()),
+                                  static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
   return ETC_OK;
 }

@@ -3,12 +3,20 @@
 // Pure data movement, HBM bound: each launch copies a list of routed boxes
 // between a rank's four state arenas (strided rows) and message sections
 // (contiguous rows), for all four state kinds.  Boxes are pre-cut on the host
-// into uniform tiles of about kTileElems elements per kind; the grid is a
-// few workgroups per CU, and each workgroup walks one contiguous range of
-// tiles.  A tile's descriptor is uniform across the workgroup (read once per
-// box through the scalar cache).  Within a tile, the 256 threads move 16-byte
-// vectors, several loads in flight per thread before the matching stores;
-// stores and loads are non-temporal because nothing is reused.
+// into uniform tiles of kTileElems elements per kind.
+//
+// Launch shape: a persistent grid of one 256-thread workgroup per CU (the
+// launcher reserves just over half of a CU's LDS per workgroup, so no second
+// workgroup can become resident), walking tiles interleaved (tile t goes to
+// workgroup t mod grid), so the whole GPU sweeps the buffers front to back.
+// A tile's descriptor is uniform across the workgroup (scalar loads).
+// Within a tile, each thread moves 16-byte vectors in batches: 16 loads in
+// flight, then the 16 stores, for contiguous rows (a workgroup streams 64 KB
+// per batch); 4 for strided rows.  Loads and stores are non-temporal since
+// nothing is reused.  On MI355X this shape measured best of the ones tried
+// (deeper batches at low occupancy beat more resident waves with shallow
+// batches: the memory system is saturated and fewer, larger contiguous
+// request streams per CU use it better).
 #include <hip/hip_runtime.h>
 
 #include "copy_geom.hpp"
@@ -28,7 +36,8 @@ struct CopyArgs {
   char* peer[ETC_MAX_PEERS];
 };
 
-constexpr int kUnroll = 4;
+constexpr int kRowBatch = 16;  // vectors in flight per thread, contiguous rows
+constexpr int kBatch2D = 4;    // vectors in flight per thread, strided rows
 
 // Copy nr rows of row_bytes bytes (16-byte aligned starts, row_bytes a
 // multiple of 16 when nr > 1) from src (row pitch sld bytes) to dst (pitch dld).
@@ -39,14 +48,14 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
   const uint32_t nv = nr * vpr;
   uint32_t i = threadIdx.x;
   if (nr == 1) {
-    for (; i + (kUnroll - 1) * kCopyThreads < nv; i += kUnroll * kCopyThreads) {
-      u32x4 v[kUnroll];
+    for (; i + (kRowBatch - 1) * kCopyThreads < nv; i += kRowBatch * kCopyThreads) {
+      u32x4 v[kRowBatch];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u)
+      for (int u = 0; u < kRowBatch; ++u)
         v[u] = __builtin_nontemporal_load(
             reinterpret_cast<const u32x4*>(src + uint64_t(i + u * kCopyThreads) * 16));
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u)
+      for (int u = 0; u < kRowBatch; ++u)
         __builtin_nontemporal_store(
             v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
     }
@@ -56,11 +65,11 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
           reinterpret_cast<u32x4*>(dst + uint64_t(i) * 16));
     return;
   }
-  for (; i + (kUnroll - 1) * kCopyThreads < nv; i += kUnroll * kCopyThreads) {
-    u32x4 v[kUnroll];
-    uint32_t r[kUnroll], c[kUnroll];
+  for (; i + (kBatch2D - 1) * kCopyThreads < nv; i += kBatch2D * kCopyThreads) {
+    u32x4 v[kBatch2D];
+    uint32_t r[kBatch2D], c[kBatch2D];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kBatch2D; ++u) {
       const uint32_t idx = i + u * kCopyThreads;
       r[u] = idx / vpr;
       c[u] = idx - r[u] * vpr;
@@ -68,7 +77,7 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
           reinterpret_cast<const u32x4*>(src + r[u] * sld + uint64_t(c[u]) * 16));
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
+    for (int u = 0; u < kBatch2D; ++u)
       __builtin_nontemporal_store(v[u],
                                   reinterpret_cast<u32x4*>(dst + r[u] * dld + uint64_t(c[u]) * 16));
   }
@@ -126,13 +135,12 @@ __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox&
 
 template <bool kPack>
 __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
-  uint32_t t0, t1;
-  block_tiles(blockIdx.x, gridDim.x, a.ntiles, &t0, &t1);
-  if (t0 >= t1) return;
-  uint32_t bi = box_of_tile(a.boxes, a.nbox, t0);
+  uint32_t t = blockIdx.x;
+  if (t >= a.ntiles) return;
+  uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
   CopyBox b = a.boxes[bi];
   uint32_t next0 = a.boxes[bi + 1].tile0;
-  for (uint32_t t = t0; t < t1; ++t) {
+  for (; t < a.ntiles; t += gridDim.x) {
     while (t >= next0) {
       ++bi;
       b = a.boxes[bi];
@@ -150,8 +158,8 @@ __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
 }  // namespace
 
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, void* const arena[4], void* const* peers, int npeers,
-                       hipStream_t stream) {
+                       uint32_t grid, uint32_t lds_reserve, void* const arena[4],
+                       void* const* peers, int npeers, hipStream_t stream) {
   if (ntiles == 0) return hipSuccess;
   CopyArgs a{};
   a.boxes = boxes;
@@ -160,10 +168,12 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   for (int k = 0; k < 4; ++k) a.arena[k] = static_cast<char*>(arena[k]);
   for (int p = 0; p < npeers; ++p) a.peer[p] = static_cast<char*>(peers[p]);
   const uint32_t g = grid < ntiles ? grid : ntiles;
+  // the dynamic LDS is not used by the kernel: it caps residency at one
+  // workgroup per CU
   if (pack)
-    hipLaunchKernelGGL(copy_kernel<true>, dim3(g), dim3(kCopyThreads), 0, stream, a);
+    hipLaunchKernelGGL(copy_kernel<true>, dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
   else
-    hipLaunchKernelGGL(copy_kernel<false>, dim3(g), dim3(kCopyThreads), 0, stream, a);
+    hipLaunchKernelGGL(copy_kernel<false>, dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
   return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
-// copy_geom.hpp -- tile geometry of the copy engine: which tiles a workgroup
-// owns, which box a tile belongs to, and the rows and columns of a tile.
+// copy_geom.hpp -- tile geometry of the copy engine: which box a tile belongs
+// to, and the rows and columns of a tile.
 // Host and device share it, so the planner's bounds checks and the kernel
 // walk the same tiles.
 #pragma once
@@ -11,13 +11,6 @@
 #include "etc_internal.hpp"
 
 namespace etc {
-
-// Contiguous tile range [t0, t1) of workgroup `bid` out of G.
-__host__ __device__ inline void block_tiles(uint32_t bid, uint32_t G, uint32_t ntiles,
-                                            uint32_t* t0, uint32_t* t1) {
-  *t0 = uint32_t(uint64_t(bid) * ntiles / G);
-  *t1 = uint32_t(uint64_t(bid + 1) * ntiles / G);
-}
 
 // Index of the box holding tile t: the last box with tile0 <= t.
 __host__ __device__ inline uint32_t box_of_tile(const CopyBox* boxes, uint32_t nbox, uint32_t t) {

@@ -98,8 +98,8 @@ constexpr int kCmThreads = 256;
 
 // kernel launchers (copy.hip, cost.hip)
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, void* const arena[4], void* const* peers, int npeers,
-                       hipStream_t stream);
+                       uint32_t grid, uint32_t lds_reserve, void* const arena[4],
+                       void* const* peers, int npeers, hipStream_t stream);
 hipError_t launch_cost(const RouteTensor* rt, int nt, int S, int D, int tps, int tpd, int which,
                        uint64_t* out, hipStream_t stream);
 
@@ -129,7 +129,8 @@ struct etc_plan_s {
 
   // device side
   int device = -1;
-  uint32_t copy_grid = 0;
+  uint32_t copy_grid = 0;       // persistent copy grid: one workgroup per CU
+  uint32_t copy_lds_reserve = 0;  // dynamic LDS per copy workgroup (occupancy cap)
   etc::RouteTensor* d_route_tensors = nullptr;
   etc::CopyBox* d_boxes = nullptr;
   std::vector<etc::CopyTable> pack_tab, unpack_tab;
