@@ -3,9 +3,12 @@
 One step = the cost matrices (ROUTE and the paper's COST) + one source rank's
 pack + one target rank's unpack, at real shape, with every input resident in
 HBM before the timed region.  Other sources feeding the target are packed
-once during set-up (their packs belong to other GPUs).
+once during set-up (their packs belong to other GPUs).  New ranks are paired
+with old ranks by the optimal migration sketch (ETC_PLAN_SKETCH; --identity
+pairs rank d with rank d); the share is process 0's: the old rank it packs
+and the new rank it becomes.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--identity]
 
 Prints one JSON line: value = algorithmic bytes of pack + unpack (each reads
 and writes its routed bytes) per step time, in GB/s; the roofline object is for
@@ -57,22 +60,27 @@ def measured_traffic(workload, kernel, algorithmic):
     return ent.get("bytes_per_launch")
 
 
-def cpu_baseline(w, plan):
+def cpu_baseline(w, identity):
     """The oracle (as it stands, one thread) on the tensors of layer 0 of the
     same share: materialize + cut for the unpack target and the pack source's
-    messages.  Reported in GB/s over the sample's algorithmic bytes."""
+    messages, routed with the oracle's own migration sketch (or the identity
+    pairing).  Reported in GB/s over the sample's algorithmic bytes."""
     import numpy as np
 
     import oracle
     import synth
 
     m, a, b = w.model, w.src, w.dst
+    pair = None if identity else oracle.sketch(oracle.matrices(m, a, b)["cost"])[0]
     T = oracle.tensors(m)
     sample = [i for i, t in enumerate(T) if t["layer"] == 0]
     t_lo, t_hi = sample[0], sample[-1] + 1
-    s0, d0 = w.pack_rank, w.unpack_rank
+    s0 = w.pack_rank
+    d0 = w.unpack_rank if pair is None else next((d for d in range(b.world) if pair[d] == s0),
+                                                  w.unpack_rank)
     feeders = sorted({s for s in range(a.world)
-                      if any(x["tensor"] in sample for x in oracle.message(m, a, b, s, d0)[0])} | {s0})
+                      if any(x["tensor"] in sample
+                             for x in oracle.message(m, a, b, s, d0, pair=pair)[0])} | {s0})
     fc = {i: t["cols"] for i, t in enumerate(T)}
     src = {}
     for s in feeders:
@@ -80,14 +88,14 @@ def cpu_baseline(w, plan):
         src[s] = [np.zeros(elems * e, np.uint8) for e in (2, 4, 4, 4)]
         synth.fill_host([p for p in pieces if t_lo <= p["tensor"] < t_hi], fc, src[s], w.seed)
     dst = {d0: [np.zeros(oracle.layout(m, b, d0)[1] * e, np.uint8) for e in (2, 4, 4, 4)]}
-    send = {s0: np.zeros(oracle.send_layout(m, a, b, s0)[3], np.uint8)}
-    sent = sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"])
-               for d in range(b.world) for x in oracle.message(m, a, b, s0, d)[0] if x["tensor"] in sample)
-    got = sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"])
-              for s in range(a.world) for x in oracle.message(m, a, b, s, d0)[0] if x["tensor"] in sample)
+    send = {s0: np.zeros(oracle.send_layout(m, a, b, s0, pair=pair)[3], np.uint8)}
+    sent = sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"]) for d in range(b.world)
+               for x in oracle.message(m, a, b, s0, d, pair=pair)[0] if x["tensor"] in sample)
+    got = sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"]) for s in range(a.world)
+              for x in oracle.message(m, a, b, s, d0, pair=pair)[0] if x["tensor"] in sample)
     alg = 2 * sent + 2 * got
     t0 = time.perf_counter()
-    oracle.migrate(m, a, b, src, dst, send, t_lo, t_hi)
+    oracle.migrate(m, a, b, src, dst, send, t_lo, t_hi, pair=pair)
     dt = time.perf_counter() - t0
     return {"value": round(alg / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"tensors of layer 0 ({len(sample)} tensors): pack of source {s0} + unpack of "
@@ -101,6 +109,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama-70b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--identity", action="store_true", help="identity pairing instead of the sketch")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the migration; runs on more than one GPU "
@@ -121,12 +130,15 @@ def main():
     s0, d0 = w.pack_rank, w.unpack_rank
 
     t0 = time.perf_counter()
-    plan = etc.etc_plan(w.model, w.src, w.dst)
+    plan = etc.etc_plan(w.model, w.src, w.dst, flags=0 if args.identity else etc.PLAN_SKETCH)
     plan_ms = (time.perf_counter() - t0) * 1e3
     S, D = plan.S, plan.D
     if w.mode == "full":  # every source packs, every target unpacks
         packers, unpackers = list(range(S)), list(range(D))
-    else:  # one source's pack and one target's unpack
+    else:  # process 0's share: the old rank it packs, the new rank it becomes
+        s0, d0 = plan.process(w.pack_rank)
+        if d0 < 0:
+            d0 = w.unpack_rank
         packers, unpackers = [s0], [d0]
     feeders = sorted({int(s) for d in unpackers for s in np.nonzero(plan.recv_counts(d))[0]})
     resident = sorted(set(feeders) | set(packers))
@@ -195,6 +207,15 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     cm_us = e0.elapsed_time(e1) * 1e3 / 20
+    # the migration sketch on the host (Hungarian on COST), as the paper times
+    # it together with the cost matrix
+    cost_host = cost.cpu().numpy().view(np.uint64).reshape(D, S)
+    ts = []
+    for _ in range(5):
+        t1 = time.perf_counter()
+        etc.etc_sketch(cost_host)
+        ts.append(time.perf_counter() - t1)
+    sketch_us = sorted(ts)[2] * 1e6
 
     # practical ceiling: a plain device-to-device copy of the unpack's bytes
     nb = unpack_bytes // 2
@@ -223,13 +244,16 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "src": f"TP{w.src.tp}xPP{w.src.pp}",
-                   "dst": f"TP{w.dst.tp}xPP{w.dst.pp}", "pack_ranks": packers,
+                   "dst": f"TP{w.dst.tp}xPP{w.dst.pp}",
+                   "pairing": "identity" if args.identity else "migration sketch",
+                   "pack_ranks": packers,
                    "unpack_ranks": unpackers, "alg_bytes_per_step": alg_bytes},
         "frac_of_peak": round(value / PEAK_HBM_GBPS, 4),
         "pack_GBps": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1),
         "unpack_GBps": round(unpack_bytes / (unpack_ms * 1e-3) / 1e9, 1),
         "pack_ms": round(pack_ms, 4), "unpack_ms": round(unpack_ms, 4),
         "cost_matrix_us": round(cm_us, 2), "cost_matrix_cells": S * D,
+        "sketch_us": round(sketch_us, 1), "pairing": "identity" if args.identity else "sketch",
         "d2d_copy_GBps": round(d2d_gbps, 1), "plan_ms": round(plan_ms, 2),
         "roofline": {"bound": "hbm", "kernel": f"copy_kernel ({dom[0]})",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -238,7 +262,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle, one thread) ...")
-        out["cpu_baseline"] = cpu_baseline(w, plan)
+        out["cpu_baseline"] = cpu_baseline(w, args.identity)
     print(json.dumps(out), flush=True)
 
 

@@ -18,6 +18,7 @@
  *     states of every workload type move together: bf16 parameter, fp32
  *     master, fp32 Adam m, fp32 Adam v (Sec. III-D).
  * This library is the data-parallel hot path of that migration on one GPU:
+ *   etc_sketch      host: the migration sketch (pairing of new and old ranks)
  *   etc_plan        host: layouts, routing, message layout, tile tables
  *   etc_cost_matrix device: byte matrices over every (source, target) pair
  *   etc_pack        device: a source rank's shards -> one message per peer
@@ -83,10 +84,12 @@ enum { ETC_KIND_PARAM_BF16 = 0, ETC_KIND_MASTER_F32 = 1, ETC_KIND_ADAM_M_F32 = 2
 /* Matrix selectors for etc_cost_matrix (all values in bytes, over the four
  * state kinds = 14 bytes per element):
  *  ROUTE            S x D: bytes source s sends to target d.  Each target
- *                   element is sent once.  Target d keeps what source rank d
- *                   already holds (Refer).  Any other element comes from the
- *                   holder with the smallest key (copy role differs,
- *                   tp_s != tp_d mod TP_src, pp_s, tp_s).
+ *                   element is sent once.  Target d keeps what its paired
+ *                   source (the same GPU in the migration sketch; source d
+ *                   under the identity pairing) already holds (Refer).  Any
+ *                   other element comes from the holder with the smallest
+ *                   key (copy role differs, tp_s != tp_d mod TP_src, pp_s,
+ *                   tp_s).
  *  OVERLAP          S x D: bytes of (held by s) intersect (needed by d), by
  *                   logical identity (a replica counts as held).
  *  OVERLAP_SHARDED  S x D: OVERLAP over tensors with exactly one copy in both
@@ -101,8 +104,10 @@ enum { ETC_ALL_RANKS = -1 };
 enum { ETC_SIDE_SRC = 0, ETC_SIDE_DST = 1 };
 
 /* etc_plan flags */
-enum { ETC_PLAN_HOST_ONLY = 1 /* build host tables only: no device memory, no
-                                 device calls allowed on this plan */ };
+enum { ETC_PLAN_HOST_ONLY = 1, /* build host tables only: no device memory, no
+                                  device calls allowed on this plan */
+       ETC_PLAN_SKETCH = 2     /* pair new and old ranks with the optimal
+                                  migration sketch (etc_sketch on COST) */ };
 
 enum {
   ETC_OK = 0,
@@ -146,20 +151,47 @@ typedef struct {
                               c1 - c0                                      */
 } etc_piece_info;
 
+/* Migration sketch (Sec. III-B, objective Eq. (2), constraints Eq. (3) for
+ * M > N and Eq. (4) for M <= N, Algorithm 1): given an M x N cost matrix
+ * (host memory, row-major, rows = new ranks, columns = old ranks, as COST
+ * from etc_cost_matrix), pair rows with columns so the summed cost is
+ * minimal: pad to k x k with zeros (k = max(M, N)), solve the square
+ * assignment problem, drop pairs in the padding.  Output pair[i] (M entries,
+ * host) = the column paired with row i, or -1; *total (may be NULL) = the
+ * kept pairs' summed cost.  Several optimal pairings may exist; any one is
+ * returned.  Entries must be below 2^52.  Host only, O(k^3).
+ * Errors: INVALID_ARG, UNSUPPORTED, NOMEM. */
+ETC_API int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* total);
+
 /* Build a migration plan from `model`, the old configuration `src` and the new
  * configuration `dst` (Sec. III: the primitive's inputs are the two parallel
- * configurations and the model).  Host work: the logical tensor table, every
- * rank's layout, the routing of every target element, every message layout.
- * Device tables (routed boxes cut into uniform tiles, and the tensor table for
- * etc_cost_matrix) are built for source rank `rank` and target rank `rank`
- * (a process is both the old and the new owner of its GPU), or for all ranks
- * with ETC_ALL_RANKS, and copied to the current device, which the plan is
- * then bound to.  With ETC_PLAN_HOST_ONLY no device memory is touched.
+ * configurations and the model), with new ranks paired to old ranks by
+ * `pair` (D entries, host: pair[d] = the old rank whose GPU becomes new rank
+ * d, or -1 for a new GPU; each old rank at most once), or by the identity
+ * pairing when pair is NULL, or by the optimal sketch with ETC_PLAN_SKETCH.
+ * Host work: the logical tensor table, every rank's layout, the routing of
+ * every target element, every message layout.
+ * `rank` names a process: process p < S holds old rank p and becomes the new
+ * rank paired with it (if any); processes S, S+1, ... are new GPUs and take
+ * the unpaired new ranks in ascending order (etc_plan_process reports both
+ * roles).  Device tables (routed boxes cut into uniform tiles, the tensor
+ * table and the pairing for etc_cost_matrix) are built for that process's
+ * pack and unpack, or for every rank with ETC_ALL_RANKS, and copied to the
+ * current device, which the plan is then bound to.  With ETC_PLAN_HOST_ONLY
+ * no device memory is touched.
  * On success *out owns host and device memory until etc_plan_free.
- * Errors: INVALID_ARG, INDIVISIBLE, UNSUPPORTED (dp != 1, GPT with GQA),
- * RANK, NOMEM, HIP. */
+ * Errors: INVALID_ARG (also a bad pairing), INDIVISIBLE, UNSUPPORTED (dp != 1,
+ * GPT with GQA), RANK, NOMEM, HIP. */
 ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
-             const etc_parallel_cfg* dst, int rank, uint32_t flags, etc_plan_t** out);
+                     const etc_parallel_cfg* dst, const int32_t* pair, int rank, uint32_t flags,
+                     etc_plan_t** out);
+
+/* The plan's pairing: pair[d] (D entries) = old rank paired with new rank d, or -1. */
+ETC_API int etc_plan_pairing(const etc_plan_t* plan, int32_t* pair);
+
+/* Roles of process `process` (see etc_plan): the old rank it holds and the
+ * new rank it becomes, each -1 if none.  Errors: INVALID_ARG, RANK. */
+ETC_API int etc_plan_process(const etc_plan_t* plan, int process, int* src_rank, int* dst_rank);
 
 /* Release a plan (NULL is a no-op).  Device work using it must be complete. */
 ETC_API void etc_plan_free(etc_plan_t* plan);
@@ -201,7 +233,7 @@ ETC_API int etc_cost_matrix(const etc_plan_t* plan, int which, uint64_t* d_out, 
  * total bytes): one contiguous message per target peer, the Send side of
  * Sec. III-D.  Every message byte is written (box padding is zero); other
  * bytes of send_buf are not touched.
- * Errors: INVALID_ARG, RANK (src_rank not built into the plan), ALIGN, HIP. */
+ * Errors: INVALID_ARG, RANK (src_rank's tables not built into the plan), ALIGN, HIP. */
 ETC_API int etc_pack(const etc_plan_t* plan, int src_rank, const void* const src_arena[4],
              void* send_buf, void* stream);
 

@@ -83,13 +83,14 @@ def lib():
         L.orc_tensor_get.argtypes = [mp, ctypes.c_int, ctypes.POINTER(Tensor)]
         L.orc_layout.argtypes = [mp, cp, ctypes.c_int, ctypes.POINTER(Piece), ctypes.c_int, u64p]
         for f in (L.orc_matrices, L.orc_matrices_bruteforce):
-            f.argtypes = [mp, cp, cp, vp, vp, vp, vp]
-        L.orc_send_layout.argtypes = [mp, cp, cp, ctypes.c_int, vp, vp, vp, u64p]
-        L.orc_message.argtypes = [mp, cp, cp, ctypes.c_int, ctypes.c_int, ctypes.POINTER(MBox),
+            f.argtypes = [mp, cp, cp, vp, vp, vp, vp, vp]
+        L.orc_send_layout.argtypes = [mp, cp, cp, vp, ctypes.c_int, vp, vp, vp, u64p]
+        L.orc_message.argtypes = [mp, cp, cp, vp, ctypes.c_int, ctypes.c_int, ctypes.POINTER(MBox),
                                   ctypes.c_int, u64p]
-        L.orc_migrate.argtypes = [mp, cp, cp, vp, vp, vp, ctypes.c_int, ctypes.c_int]
-        L.orc_dst_origin.argtypes = [mp, cp, cp, ctypes.c_int, vp, ctypes.c_int64, vp, vp]
-        L.orc_msg_origin.argtypes = [mp, cp, cp, ctypes.c_int, ctypes.c_int, vp, ctypes.c_int64, vp]
+        L.orc_migrate.argtypes = [mp, cp, cp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int]
+        L.orc_dst_origin.argtypes = [mp, cp, cp, vp, ctypes.c_int, vp, ctypes.c_int64, vp, vp]
+        L.orc_msg_origin.argtypes = [mp, cp, cp, vp, ctypes.c_int, ctypes.c_int, vp, ctypes.c_int64, vp]
+        L.orc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
         _lib = L
     return _lib
 
@@ -110,6 +111,15 @@ def _check(rc, what):
 
 def _ptr(a):
     return ctypes.c_void_p(a.ctypes.data) if a is not None else ctypes.c_void_p(0)
+
+
+def _pair(pair):
+    """Pairing (new rank -> old rank or -1) as an int32 array, or None for the
+    identity pairing.  Keeps the array alive with the returned pointer."""
+    if pair is None:
+        return None, ctypes.c_void_p(0)
+    a = np.ascontiguousarray(pair, np.int32)
+    return a, ctypes.c_void_p(a.ctypes.data)
 
 
 def tensors(model):
@@ -138,7 +148,7 @@ def layout(model, cfg, rank):
             for p in arr[:n]], elems.value
 
 
-def matrices(model, src, dst, brute=False):
+def matrices(model, src, dst, brute=False, pair=None):
     """dict route (SxD), overlap (SxD), overlap_sharded (SxD), cost (DxS), bytes."""
     S, D = src.world, dst.world
     r = np.zeros((S, D), np.uint64)
@@ -147,12 +157,13 @@ def matrices(model, src, dst, brute=False):
     cst = np.zeros((D, S), np.uint64)
     f = lib().orc_matrices_bruteforce if brute else lib().orc_matrices
     m, a, b = _m(model), _c(src), _c(dst)
-    _check(f(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), _ptr(r), _ptr(o), _ptr(osh),
+    keep, pp = _pair(pair)
+    _check(f(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, _ptr(r), _ptr(o), _ptr(osh),
              _ptr(cst)), "matrices")
     return dict(route=r, overlap=o, overlap_sharded=osh, cost=cst)
 
 
-def send_layout(model, src, dst, s):
+def send_layout(model, src, dst, s, pair=None):
     """(counts, padded, displs, total) in bytes for source s."""
     D = dst.world
     cnt = np.zeros(D, np.uint64)
@@ -160,25 +171,28 @@ def send_layout(model, src, dst, s):
     dsp = np.zeros(D, np.uint64)
     tot = ctypes.c_uint64()
     m, a, b = _m(model), _c(src), _c(dst)
-    _check(lib().orc_send_layout(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), s, _ptr(cnt),
-                                 _ptr(pad), _ptr(dsp), ctypes.byref(tot)), "send_layout")
+    keep, pp = _pair(pair)
+    _check(lib().orc_send_layout(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s,
+                                 _ptr(cnt), _ptr(pad), _ptr(dsp), ctypes.byref(tot)), "send_layout")
     return cnt, pad, dsp, tot.value
 
 
-def message(model, src, dst, s, d):
+def message(model, src, dst, s, d, pair=None):
     """(boxes, npad): the boxes of message s->d in order, and the section length."""
     m, a, b = _m(model), _c(src), _c(dst)
     npad = ctypes.c_uint64()
-    n = _check(lib().orc_message(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), s, d, None, 0,
-                                 ctypes.byref(npad)), "message")
+    keep, pp = _pair(pair)
+    n = _check(lib().orc_message(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d, None,
+                                 0, ctypes.byref(npad)), "message")
     arr = (MBox * max(n, 1))()
-    _check(lib().orc_message(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), s, d, arr, n,
+    _check(lib().orc_message(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d, arr, n,
                              ctypes.byref(npad)), "message")
     return [dict(tensor=x.tensor, role_d=x.role_d, r0=x.r0, r1=x.r1, c0=x.c0, c1=x.c1, moff=x.moff)
             for x in arr[:n]], npad.value
 
 
-def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0, t_hi=-1):
+def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0, t_hi=-1,
+            pair=None):
     """Materialize-then-reslice.  src_arenas: {rank: [4 uint8 arrays]} (resident
     sources); dst_arenas: {rank: [4 uint8 arrays]} to fill; send_bufs:
     {rank: uint8 array} to fill with that source's messages."""
@@ -195,28 +209,42 @@ def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0
     for s, arr in (send_bufs or {}).items():
         sb[s] = arr.ctypes.data
     m, a, b = _m(model), _c(src), _c(dst)
-    _check(lib().orc_migrate(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b),
+    keep, pp = _pair(pair)
+    _check(lib().orc_migrate(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp,
                              ctypes.cast(sa, ctypes.c_void_p), ctypes.cast(da, ctypes.c_void_p),
                              ctypes.cast(sb, ctypes.c_void_p), t_lo, t_hi), "migrate")
 
 
-def dst_origin(model, src, dst, d, offs):
+def dst_origin(model, src, dst, d, offs, pair=None):
     """(src_rank int32[n], src_off uint64[n]) for destination arena element offsets."""
     offs = np.ascontiguousarray(offs, np.uint64)
     rk = np.zeros(offs.size, np.int32)
     so = np.zeros(offs.size, np.uint64)
     m, a, b = _m(model), _c(src), _c(dst)
-    _check(lib().orc_dst_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), d, _ptr(offs),
-                                offs.size, _ptr(rk), _ptr(so)), "dst_origin")
+    keep, pp = _pair(pair)
+    _check(lib().orc_dst_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, d,
+                                _ptr(offs), offs.size, _ptr(rk), _ptr(so)), "dst_origin")
     return rk, so
 
 
-def msg_origin(model, src, dst, s, d, pos):
+def msg_origin(model, src, dst, s, d, pos, pair=None):
     """Source-arena element offsets for element positions inside a kind section
     of message s->d (UINT64_MAX for padding)."""
     pos = np.ascontiguousarray(pos, np.uint64)
     so = np.zeros(pos.size, np.uint64)
     m, a, b = _m(model), _c(src), _c(dst)
-    _check(lib().orc_msg_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), s, d,
+    keep, pp = _pair(pair)
+    _check(lib().orc_msg_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d,
                                 _ptr(pos), pos.size, _ptr(so)), "msg_origin")
     return so
+
+
+def sketch(cost):
+    """Migration sketch of a cost matrix (rows = new ranks, columns = old ranks):
+    (pair int32[M] with the old rank paired to each new rank or -1, total cost)."""
+    c = np.ascontiguousarray(cost, np.uint64)
+    M, N = c.shape
+    pair = np.zeros(M, np.int32)
+    tot = ctypes.c_uint64()
+    _check(lib().orc_sketch(_ptr(c), M, N, _ptr(pair), ctypes.byref(tot)), "sketch")
+    return pair, tot.value

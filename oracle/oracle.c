@@ -293,6 +293,7 @@ typedef struct {
   orc_model m;
   orc_cfg src, dst;
   int S, D, nt;
+  int32_t* home; /* home[d]: source rank paired with target d (the same GPU), or -1 */
   orc_tensor* T;
   int* ns;           /* pieces per source rank      */
   orc_piece** ps;    /* pieces of each source rank  */
@@ -313,10 +314,14 @@ static void ctx_free(ctx_t* x) {
   free(x->s_elems);
   free(x->d_elems);
   free(x->T);
+  free(x->home);
   memset(x, 0, sizeof *x);
 }
 
-static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_cfg* dst) {
+/* pair: pair[d] = source rank paired with target d, or -1 (a migration sketch,
+ * Sec. III-B); NULL means the identity pairing (target d with source d). */
+static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_cfg* dst,
+                    const int32_t* pair) {
   memset(x, 0, sizeof *x);
   int rc = check_model(m);
   if (rc) return rc;
@@ -340,6 +345,23 @@ static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_
     return ORC_ENOMEM;
   }
   build_tensors(m, x->T);
+  x->home = calloc((size_t)x->D, sizeof(int32_t));
+  if (!x->home) {
+    ctx_free(x);
+    return ORC_ENOMEM;
+  }
+  for (int d = 0; d < x->D; ++d) {
+    x->home[d] = pair ? pair[d] : (d < x->S ? d : -1);
+    if (x->home[d] < -1 || x->home[d] >= x->S) {
+      ctx_free(x);
+      return ORC_EINVAL;
+    }
+    for (int e = 0; e < d; ++e)
+      if (x->home[d] >= 0 && x->home[e] == x->home[d]) {
+        ctx_free(x);
+        return ORC_EINVAL; /* a source can be paired with one target at most */
+      }
+  }
   for (int s = 0; s < x->S; ++s) {
     x->ns[s] = layout(m, src, x->T, x->nt, s, NULL, NULL);
     x->ps[s] = calloc((size_t)x->ns[s] + 1, sizeof(orc_piece));
@@ -367,8 +389,8 @@ static int in_box(const orc_piece* p, int64_t r, int64_t c) {
 
 /* Which source rank sends element (r, c) of tensor t to destination d that
  * needs it in copy role role_d.  The paper pairs ranks and keeps what both
- * sides of a pair hold in place (Refer); with the identity pairing, source
- * rank d keeps whatever it already holds.  Any other element has several
+ * sides of a pair hold in place (Refer): the source paired with d keeps
+ * whatever it already holds.  Any other element has several
  * possible senders only when it is replicated (TP-replicated tensors, the
  * tied embedding copy); the reading taken here picks the holder with the
  * smallest key (role differs from role_d, tp differs from tp_d mod TP_src,
@@ -376,10 +398,11 @@ static int in_box(const orc_piece* p, int64_t r, int64_t c) {
  * scale-out sources.  Holders are found by scanning every source rank's
  * pieces.  Returns -1 if no source holds the element. */
 static int sender_of_element(const ctx_t* x, int d, int role_d, int t, int64_t r, int64_t c) {
-  if (d < x->S) {
-    for (int i = 0; i < x->ns[d]; ++i) {
-      const orc_piece* p = &x->ps[d][i];
-      if (p->tensor == t && in_box(p, r, c)) return d;
+  const int h = x->home[d];
+  if (h >= 0) {
+    for (int i = 0; i < x->ns[h]; ++i) {
+      const orc_piece* p = &x->ps[h][i];
+      if (p->tensor == t && in_box(p, r, c)) return h;
     }
   }
   int pp_d, tp_d;
@@ -441,11 +464,12 @@ static int holds_item(const ctx_t* x, const orc_cfg* c, int pp, int tp, const or
 
 /* The sender rule evaluated on a whole item (all its elements share holders). */
 static int sender_of_item(const ctx_t* x, int d, int role_d, const orc_tensor* t, int64_t a) {
-  if (d < x->S) {
+  const int h = x->home[d];
+  if (h >= 0) {
     int pp, tp;
-    coords(&x->src, d, &pp, &tp);
+    coords(&x->src, h, &pp, &tp);
     if (holds_item(x, &x->src, pp, tp, t, 0, a) || holds_item(x, &x->src, pp, tp, t, 1, a))
-      return d;
+      return h;
   }
   int pp_d, tp_d;
   coords(&x->dst, d, &pp_d, &tp_d);
@@ -536,10 +560,10 @@ int orc_layout(const orc_model* m, const orc_cfg* c, int rank, orc_piece* out, i
  * COST[d][s] = bytes(d) - OVERLAP[s][d]: the paper's c_ij with rows = the new
  *   (curr) ranks and columns = the old (prev) ranks (Sec. III-B), in bytes.
  * Computed over LCM workload items (Sec. III-C).  Any output may be NULL. */
-int orc_matrices(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, uint64_t* route,
-                 uint64_t* overlap, uint64_t* overlap_sh, uint64_t* cost) {
+int orc_matrices(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+                 uint64_t* route, uint64_t* overlap, uint64_t* overlap_sh, uint64_t* cost) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   const int S = x.S, D = x.D;
   uint64_t* R = calloc((size_t)S * D, 8);
@@ -597,10 +621,10 @@ out:
 /* The same four matrices by enumerating every element of every tensor and
  * scanning every rank's pieces for it.  Tiny models only. */
 int orc_matrices_bruteforce(const orc_model* m, const orc_cfg* src, const orc_cfg* dst,
-                            uint64_t* route, uint64_t* overlap, uint64_t* overlap_sh,
-                            uint64_t* cost) {
+                            const int32_t* pair, uint64_t* route, uint64_t* overlap,
+                            uint64_t* overlap_sh, uint64_t* cost) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   const int S = x.S, D = x.D;
   uint64_t* R = calloc((size_t)S * D, 8);
@@ -720,10 +744,10 @@ static int message_boxes(const ctx_t* x, int s, int d, orc_mbox* out, uint64_t* 
  * (unpadded, = ROUTE[s][d]), the padded message bytes, and the byte
  * displacement of the message (messages in destination order, each at a
  * multiple of 256 bytes).  *total = buffer length. */
-int orc_send_layout(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, int s,
-                    uint64_t* count, uint64_t* padded, uint64_t* displ, uint64_t* total) {
+int orc_send_layout(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+                    int s, uint64_t* count, uint64_t* padded, uint64_t* displ, uint64_t* total) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   if (s < 0 || s >= x.S) {
     ctx_free(&x);
@@ -749,10 +773,10 @@ int orc_send_layout(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, 
 }
 
 /* Message s->d as a list of boxes (for tests and sampled checks). */
-int orc_message(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, int s, int d,
-                orc_mbox* out, int cap, uint64_t* npad) {
+int orc_message(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+                int s, int d, orc_mbox* out, int cap, uint64_t* npad) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   if (s < 0 || s >= x.S || d < 0 || d >= x.D) {
     ctx_free(&x);
@@ -779,11 +803,11 @@ int orc_message(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, int 
  * Full tensors are materialized from all resident sources (replicas compared
  * bit for bit), then cut.  A needed element that no resident source covers
  * is an error. */
-int orc_migrate(const orc_model* m, const orc_cfg* src, const orc_cfg* dst,
+int orc_migrate(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
                 const void* const* src_arenas, void* const* dst_arenas,
                 void* const* send_bufs, int t_lo, int t_hi) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   if (t_lo < 0) t_lo = 0;
   if (t_hi > x.nt || t_hi < 0) t_hi = x.nt;
@@ -952,10 +976,10 @@ static int find_src_piece(const ctx_t* x, int s, int t, int64_t r, int64_t c) {
 /* For destination d and arena element offsets offs[0..n): the source rank
  * whose element ends up there (by the sender rule) and that element's offset
  * in the source arena.  Gap offsets get src_rank -1. */
-int orc_dst_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, int d,
-                   const uint64_t* offs, int64_t n, int32_t* src_rank, uint64_t* src_off) {
+int orc_dst_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+                   int d, const uint64_t* offs, int64_t n, int32_t* src_rank, uint64_t* src_off) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   if (d < 0 || d >= x.D) {
     ctx_free(&x);
@@ -991,10 +1015,10 @@ int orc_dst_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, i
 /* For message s->d and element positions pos[0..n) inside a kind section:
  * the offset in source s's arena of the element stored there, or
  * UINT64_MAX for zero padding / past the end. */
-int orc_msg_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, int s, int d,
-                   const uint64_t* pos, int64_t n, uint64_t* src_off) {
+int orc_msg_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+                   int s, int d, const uint64_t* pos, int64_t n, uint64_t* src_off) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst);
+  int rc = ctx_init(&x, m, src, dst, pair);
   if (rc) return rc;
   if (s < 0 || s >= x.S || d < 0 || d >= x.D) {
     ctx_free(&x);
@@ -1031,5 +1055,91 @@ int orc_msg_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, i
   }
   free(B);
   ctx_free(&x);
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* migration sketch (Sec. III-B: indicator Eq. (1), objective Eq. (2),      */
+/* constraints Eq. (3) for M > N and Eq. (4) for M <= N, Algorithm 1)        */
+/* ------------------------------------------------------------------------ */
+
+/* Pair the M new ranks (rows of cost) with the N old ranks (columns) so the
+ * total cost of the pairs is minimal.  As Algorithm 1 does: pad the matrix
+ * with zeros to k x k, k = max(M, N), solve the square assignment problem,
+ * and drop every pair that involves a padded row or column.  The square
+ * problem is solved here as a minimum-cost flow (source -> row -> column ->
+ * sink, unit capacities) by k successive shortest augmenting paths, each
+ * found with Bellman-Ford over the residual graph.  pair[i] = the old rank
+ * paired with new rank i, or -1; *total = the kept pairs' cost. */
+int orc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* total) {
+  if (!cost || !pair || M < 1 || N < 1) return ORC_EINVAL;
+  const int k = M > N ? M : N;
+  const int V = 2 * k + 2, SRC = 0, SNK = 2 * k + 1;
+  const int E = 2 * (k * k + 2 * k);
+  int* from = calloc((size_t)E, sizeof(int));
+  int* to = calloc((size_t)E, sizeof(int));
+  int* cap = calloc((size_t)E, sizeof(int));
+  int64_t* w = calloc((size_t)E, sizeof(int64_t));
+  int64_t* dist = calloc((size_t)V, sizeof(int64_t));
+  int* via = calloc((size_t)V, sizeof(int));
+  if (!from || !to || !cap || !w || !dist || !via) {
+    free(from); free(to); free(cap); free(w); free(dist); free(via);
+    return ORC_ENOMEM;
+  }
+  int ne = 0;
+#define EDGE(a, b, c)                                          \
+  do {                                                         \
+    from[ne] = (a); to[ne] = (b); cap[ne] = 1; w[ne] = (c); ++ne;  \
+    from[ne] = (b); to[ne] = (a); cap[ne] = 0; w[ne] = -(c); ++ne; \
+  } while (0)
+  for (int i = 0; i < k; ++i) EDGE(SRC, 1 + i, 0);
+  for (int i = 0; i < k; ++i)
+    for (int j = 0; j < k; ++j) {
+      const int64_t c = (i < M && j < N) ? (int64_t)cost[(size_t)i * N + j] : 0; /* zero padding */
+      EDGE(1 + i, 1 + k + j, c);
+    }
+  for (int j = 0; j < k; ++j) EDGE(1 + k + j, SNK, 0);
+#undef EDGE
+  const int64_t INF = INT64_MAX / 4;
+  for (int round = 0; round < k; ++round) {
+    for (int v = 0; v < V; ++v) {
+      dist[v] = INF;
+      via[v] = -1;
+    }
+    dist[SRC] = 0;
+    for (int it = 0; it < V - 1; ++it) {
+      int changed = 0;
+      for (int e = 0; e < ne; ++e) {
+        if (!cap[e] || dist[from[e]] == INF) continue;
+        if (dist[from[e]] + w[e] < dist[to[e]]) {
+          dist[to[e]] = dist[from[e]] + w[e];
+          via[to[e]] = e;
+          changed = 1;
+        }
+      }
+      if (!changed) break;
+    }
+    if (dist[SNK] == INF) break; /* cannot happen on a complete bipartite graph */
+    for (int v = SNK; v != SRC; v = from[via[v]]) {
+      cap[via[v]] -= 1;
+      cap[via[v] ^ 1] += 1;
+    }
+  }
+  uint64_t tot = 0;
+  for (int i = 0; i < M; ++i) {
+    pair[i] = -1;
+    for (int j = 0; j < k; ++j) {
+      const int e = 2 * (k + i * k + j); /* the row i -> column j edge */
+      if (cap[e] == 0) {
+        if (j < N) {
+          pair[i] = j;
+          tot += cost[(size_t)i * N + j];
+        }
+        break;
+      }
+    }
+  }
+  if (total) *total = tot;
+  free(from); free(to); free(cap); free(w); free(dist); free(via);
   return ORC_OK;
 }

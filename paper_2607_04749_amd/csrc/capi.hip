@@ -34,14 +34,16 @@ void release_device(etc_plan_t* P) {
   if (prev != P->device) (void)hipSetDevice(P->device);
   if (P->d_boxes) (void)hipFree(P->d_boxes);
   if (P->d_route_tensors) (void)hipFree(P->d_route_tensors);
+  if (P->d_home) (void)hipFree(P->d_home);
   if (have_prev && prev != P->device) (void)hipSetDevice(prev);
   P->d_boxes = nullptr;
   P->d_route_tensors = nullptr;
+  P->d_home = nullptr;
 }
 
 int check_device_plan(const etc_plan_t* P) {
   if (!P) return fail(ETC_ERR_INVALID_ARG, "plan is NULL");
-  if (P->device < 0 || !P->d_route_tensors)
+  if (P->device < 0 || !P->d_route_tensors || !P->d_home)
     return fail(ETC_ERR_INVALID_ARG, "plan was built with ETC_PLAN_HOST_ONLY");
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
@@ -52,9 +54,33 @@ int check_device_plan(const etc_plan_t* P) {
   return ETC_OK;
 }
 
+// Roles of process p: it holds old rank p (p < S) and becomes the new rank
+// paired with it; processes S, S+1, ... take the unpaired new ranks in order.
+void process_roles(const etc_plan_t* P, int p, int* src_rank, int* dst_rank) {
+  const int S = P->src.world(), D = P->dst.world();
+  *src_rank = p < S ? p : -1;
+  *dst_rank = -1;
+  if (p < S) {
+    for (int d = 0; d < D; ++d)
+      if (P->home[d] == p) *dst_rank = d;
+    return;
+  }
+  int fresh = p - S;
+  for (int d = 0; d < D; ++d)
+    if (P->home[d] < 0 && fresh-- == 0) *dst_rank = d;
+}
+
+int num_processes(const etc_plan_t* P) {
+  int unpaired = 0;
+  for (int32_t h : P->home) unpaired += h < 0;
+  return P->src.world() + unpaired;
+}
+
 int upload(etc_plan_t* P, int rank) {
   using namespace etc;
   const int S = P->src.world(), D = P->dst.world();
+  int my_src = -1, my_dst = -1;
+  if (rank != ETC_ALL_RANKS) process_roles(P, rank, &my_src, &my_dst);
   hipError_t e = hipGetDevice(&P->device);
   if (e != hipSuccess) {
     P->device = -1;
@@ -75,7 +101,7 @@ int upload(etc_plan_t* P, int rank) {
 
   std::vector<CopyBox> all;
   for (int s = 0; s < S; ++s) {
-    if (rank != ETC_ALL_RANKS && rank != s) continue;
+    if (rank != ETC_ALL_RANKS && my_src != s) continue;
     CopyTable& t = P->pack_tab[s];
     auto v = build_pack_boxes(*P, s, &t.bytes);
     t.first = uint32_t(all.size());
@@ -85,7 +111,7 @@ int upload(etc_plan_t* P, int rank) {
     all.insert(all.end(), v.begin(), v.end());
   }
   for (int d = 0; d < D; ++d) {
-    if (rank != ETC_ALL_RANKS && rank != d) continue;
+    if (rank != ETC_ALL_RANKS && my_dst != d) continue;
     CopyTable& t = P->unpack_tab[d];
     auto v = build_unpack_boxes(*P, d, &t.peers, &t.bytes);
     t.first = uint32_t(all.size());
@@ -108,6 +134,10 @@ int upload(etc_plan_t* P, int rank) {
                   P->route_tensors.size() * sizeof(RouteTensor), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy (tensor table)");
   }
+  e = hipMalloc(&P->d_home, std::max<size_t>(1, P->home.size()) * sizeof(int32_t));
+  if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+  e = hipMemcpy(P->d_home, P->home.data(), P->home.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy (pairing)");
   return ETC_OK;
 }
 
@@ -133,12 +163,27 @@ int check_arenas(const void* const* arenas, const char* what) {
 
 extern "C" {
 
+int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* total) {
+  if (!cost || !pair) return fail(ETC_ERR_INVALID_ARG, "cost and pair must not be NULL");
+  if (M < 1 || N < 1 || M > 65536 || N > 65536) return fail(ETC_ERR_INVALID_ARG, "bad matrix shape");
+  for (size_t i = 0; i < size_t(M) * N; ++i)
+    if (cost[i] > (uint64_t(1) << 52)) return fail(ETC_ERR_UNSUPPORTED, "cost entries must be below 2^52");
+  try {
+    const uint64_t t = etc::solve_sketch(cost, M, N, pair);
+    if (total) *total = t;
+  } catch (const std::bad_alloc&) {
+    return fail(ETC_ERR_NOMEM, "host allocation failed");
+  }
+  return ETC_OK;
+}
+
 int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
-             int rank, uint32_t flags, etc_plan_t** out) {
+             const int32_t* pair, int rank, uint32_t flags, etc_plan_t** out) {
   if (!out) return fail(ETC_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (!model || !src || !dst) return fail(ETC_ERR_INVALID_ARG, "model, src and dst must not be NULL");
-  if (flags & ~uint32_t(ETC_PLAN_HOST_ONLY)) return fail(ETC_ERR_INVALID_ARG, "unknown plan flags");
+  if (flags & ~uint32_t(ETC_PLAN_HOST_ONLY | ETC_PLAN_SKETCH)) return fail(ETC_ERR_INVALID_ARG, "unknown plan flags");
+  if (pair && (flags & ETC_PLAN_SKETCH)) return fail(ETC_ERR_INVALID_ARG, "pass a pairing or ETC_PLAN_SKETCH, not both");
   std::unique_ptr<etc_plan_t> P;
   try {
     etc::validate(*model, *src, *dst);
@@ -149,8 +194,26 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
     P->rank = rank;
     P->flags = flags;
     const int S = P->src.world(), D = P->dst.world();
-    if (rank != ETC_ALL_RANKS && (rank < 0 || rank >= std::max(S, D)))
-      return fail(ETC_ERR_RANK, "rank " + std::to_string(rank) + " is neither a source nor a target rank");
+    P->tensors = etc::build_tensor_table(P->model);
+    etc::build_route_tensors(*P);
+    P->home.assign(D, -1);
+    if (flags & ETC_PLAN_SKETCH) {
+      const std::vector<uint64_t> cost = etc::host_cost_matrix(*P);
+      etc::solve_sketch(cost.data(), D, S, P->home.data());
+    } else if (pair) {
+      std::vector<char> taken(S, 0);
+      for (int d = 0; d < D; ++d) {
+        if (pair[d] < -1 || pair[d] >= S)
+          return fail(ETC_ERR_INVALID_ARG, "pair[" + std::to_string(d) + "] is not a source rank or -1");
+        if (pair[d] >= 0 && taken[pair[d]]++)
+          return fail(ETC_ERR_INVALID_ARG, "source rank " + std::to_string(pair[d]) + " is paired twice");
+        P->home[d] = pair[d];
+      }
+    } else {
+      for (int d = 0; d < D && d < S; ++d) P->home[d] = d;  // identity pairing
+    }
+    if (rank != ETC_ALL_RANKS && (rank < 0 || rank >= num_processes(P.get())))
+      return fail(ETC_ERR_RANK, "process " + std::to_string(rank) + " is out of range");
     etc::build_host_plan(*P);
     P->pack_tab.resize(S);
     P->unpack_tab.resize(D);
@@ -170,6 +233,20 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
   }
   *out = P.release();
   g_last_error.clear();
+  return ETC_OK;
+}
+
+int etc_plan_pairing(const etc_plan_t* P, int32_t* pair) {
+  if (!P || !pair) return fail(ETC_ERR_INVALID_ARG, "NULL argument");
+  for (size_t d = 0; d < P->home.size(); ++d) pair[d] = P->home[d];
+  return ETC_OK;
+}
+
+int etc_plan_process(const etc_plan_t* P, int process, int* src_rank, int* dst_rank) {
+  if (!P || !src_rank || !dst_rank) return fail(ETC_ERR_INVALID_ARG, "NULL argument");
+  if (process < 0 || process >= num_processes(P))
+    return fail(ETC_ERR_RANK, "process " + std::to_string(process) + " is out of range");
+  process_roles(P, process, src_rank, dst_rank);
   return ETC_OK;
 }
 
@@ -260,9 +337,9 @@ int etc_cost_matrix(const etc_plan_t* P, int which, uint64_t* d_out, void* strea
   if (which < ETC_CM_ROUTE || which > ETC_CM_COST) return fail(ETC_ERR_INVALID_ARG, "bad matrix selector");
   if (!d_out) return fail(ETC_ERR_INVALID_ARG, "d_out is NULL");
   if (!aligned(d_out, 8)) return fail(ETC_ERR_ALIGN, "d_out is not 8-byte aligned");
-  hipError_t e = etc::launch_cost(P->d_route_tensors, int(P->route_tensors.size()), P->src.world(),
-                                  P->dst.world(), P->src.tp, P->dst.tp, which, d_out,
-                                  static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_cost(P->d_route_tensors, int(P->route_tensors.size()), P->d_home,
+                                  P->src.world(), P->dst.world(), P->src.tp, P->dst.tp, which,
+                                  d_out, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "cost matrix launch");
   return ETC_OK;
 }

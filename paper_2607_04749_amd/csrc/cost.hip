@@ -14,13 +14,15 @@ namespace etc {
 namespace {
 
 __global__ __launch_bounds__(kCmThreads) void cost_kernel(const RouteTensor* __restrict__ T,
-                                                          int nt, int S, int D, int TPs, int TPd,
+                                                          int nt, const int32_t* __restrict__ home,
+                                                          int S, int D, int TPs, int TPd,
                                                           int which, uint64_t* __restrict__ out) {
   __shared__ uint64_t red_val[kCmThreads];
   __shared__ uint64_t red_need[kCmThreads];
   const int s = blockIdx.x / D, d = blockIdx.x % D;
   const int pp_d = d / TPd, tp_d = d % TPd;
   const int pp_s = s / TPs, tp_s = s % TPs;
+  const int home_d = home[d];
   uint64_t val = 0, need = 0;
   for (int i = threadIdx.x; i < nt; i += kCmThreads) {
     const RouteTensor t = T[i];
@@ -29,7 +31,7 @@ __global__ __launch_bounds__(kCmThreads) void cost_kernel(const RouteTensor* __r
     const Span want = shard_span(t, tp_d, TPd);
     need += uint64_t(want.len() * unit);
     if (which == ETC_CM_ROUTE) {
-      val += uint64_t(routed_span(t, s, d, S, TPs, TPd).len() * unit);
+      val += uint64_t(routed_span(t, s, d, home_d, TPs, TPd).len() * unit);
     } else {
       if (role_on(t.src_stage, pp_s) < 0) continue;
       if (which == ETC_CM_OVERLAP_SHARDED && !t.single_copy) continue;
@@ -59,10 +61,10 @@ __global__ __launch_bounds__(kCmThreads) void cost_kernel(const RouteTensor* __r
 
 }  // namespace
 
-hipError_t launch_cost(const RouteTensor* rt, int nt, int S, int D, int tps, int tpd, int which,
-                       uint64_t* out, hipStream_t stream) {
+hipError_t launch_cost(const RouteTensor* rt, int nt, const int32_t* home, int S, int D, int tps,
+                       int tpd, int which, uint64_t* out, hipStream_t stream) {
   hipLaunchKernelGGL(cost_kernel, dim3(unsigned(S) * unsigned(D)), dim3(kCmThreads), 0, stream,
-                     rt, nt, S, D, tps, tpd, which, out);
+                     rt, nt, home, S, D, tps, tpd, which, out);
   return hipGetLastError();
 }
 

@@ -100,8 +100,8 @@ constexpr int kCmThreads = 256;
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
                        uint32_t grid, uint32_t lds_reserve, void* const arena[4],
                        void* const* peers, int npeers, hipStream_t stream);
-hipError_t launch_cost(const RouteTensor* rt, int nt, int S, int D, int tps, int tpd, int which,
-                       uint64_t* out, hipStream_t stream);
+hipError_t launch_cost(const RouteTensor* rt, int nt, const int32_t* home, int S, int D, int tps,
+                       int tpd, int which, uint64_t* out, hipStream_t stream);
 
 }  // namespace etc
 
@@ -114,6 +114,7 @@ struct etc_plan_s {
   std::vector<etc::LogicalTensor> tensors;
   std::vector<etc::RouteTensor> route_tensors;
   std::vector<etc::RankLayout> src_layout, dst_layout;
+  std::vector<int32_t> home;  // [d]: source rank paired with target d (migration sketch), or -1
 
   // messages, indexed [s * D + d]
   struct MsgBox {
@@ -132,6 +133,7 @@ struct etc_plan_s {
   uint32_t copy_grid = 0;       // persistent copy grid: one workgroup per CU
   uint32_t copy_lds_reserve = 0;  // dynamic LDS per copy workgroup (occupancy cap)
   etc::RouteTensor* d_route_tensors = nullptr;
+  int32_t* d_home = nullptr;  // device copy of home (D entries)
   etc::CopyBox* d_boxes = nullptr;
   std::vector<etc::CopyTable> pack_tab, unpack_tab;
 };

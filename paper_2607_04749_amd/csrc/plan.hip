@@ -233,31 +233,13 @@ void build_host_plan(etc_plan_t& P) {
   P.tensors = build_tensor_table(m);
   const int nt = int(P.tensors.size());
   const int S = P.src.world(), D = P.dst.world();
+  if (int(P.home.size()) != D) fail(ETC_ERR_INVALID_ARG, "internal: pairing not set");
   P.src_layout.resize(S);
   P.dst_layout.resize(D);
   for (int s = 0; s < S; ++s) P.src_layout[s] = build_layout(P.tensors, P.src, m.num_layers, s);
   for (int d = 0; d < D; ++d) P.dst_layout[d] = build_layout(P.tensors, P.dst, m.num_layers, d);
 
-  P.route_tensors.resize(nt);
-  for (int i = 0; i < nt; ++i) {
-    const LogicalTensor& t = P.tensors[i];
-    RouteTensor& r = P.route_tensors[i];
-    r.rows = t.rows;
-    r.cols = t.cols;
-    r.split = t.split;
-    int copies_src = 0, copies_dst = 0;
-    for (int role = 0; role < 2; ++role) {
-      r.src_stage[role] = stage_of(t, role, P.src, m.num_layers);
-      r.dst_stage[role] = stage_of(t, role, P.dst, m.num_layers);
-      copies_src += r.src_stage[role] >= 0;
-      copies_dst += r.dst_stage[role] >= 0;
-    }
-    if (t.split == kRepl) {
-      copies_src *= P.src.tp;
-      copies_dst *= P.dst.tp;
-    }
-    r.single_copy = copies_src == 1 && copies_dst == 1;
-  }
+  if (P.route_tensors.size() != size_t(nt)) build_route_tensors(P);
 
   // Route every target piece: per target rank, per piece in arena order, the
   // sources that send part of it.  Messages list boxes in that order.
@@ -269,7 +251,7 @@ void build_host_plan(etc_plan_t& P) {
       const RouteTensor& rt = P.route_tensors[q.tensor];
       uint64_t got = 0;
       for (int s = 0; s < S; ++s) {
-        const Span x = routed_span(rt, s, d, S, P.src.tp, P.dst.tp);
+        const Span x = routed_span(rt, s, d, P.home[d], P.src.tp, P.dst.tp);
         if (x.len() == 0) continue;
         etc_plan_s::MsgBox b{};
         b.tensor = q.tensor;
@@ -369,6 +351,55 @@ std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<
   v.push_back(sentinel);
   if (bytes) *bytes = moved;
   return v;
+}
+
+void build_route_tensors(etc_plan_t& P) {
+  const int nt = int(P.tensors.size());
+  P.route_tensors.resize(nt);
+  for (int i = 0; i < nt; ++i) {
+    const LogicalTensor& t = P.tensors[i];
+    RouteTensor& r = P.route_tensors[i];
+    r.rows = t.rows;
+    r.cols = t.cols;
+    r.split = t.split;
+    int copies_src = 0, copies_dst = 0;
+    for (int role = 0; role < 2; ++role) {
+      r.src_stage[role] = stage_of(t, role, P.src, P.model.num_layers);
+      r.dst_stage[role] = stage_of(t, role, P.dst, P.model.num_layers);
+      copies_src += r.src_stage[role] >= 0;
+      copies_dst += r.dst_stage[role] >= 0;
+    }
+    if (t.split == kRepl) {
+      copies_src *= P.src.tp;
+      copies_dst *= P.dst.tp;
+    }
+    r.single_copy = copies_src == 1 && copies_dst == 1;
+  }
+}
+
+std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P) {
+  // COST[d][s] = bytes(d) - OVERLAP[s][d], the same interval arithmetic as
+  // the cost kernel, on the host (feeds the migration sketch at plan time)
+  const int S = P.src.world(), D = P.dst.world();
+  std::vector<uint64_t> cost(size_t(D) * S, 0);
+  for (int d = 0; d < D; ++d) {
+    const int pp_d = d / P.dst.tp, tp_d = d % P.dst.tp;
+    for (int s = 0; s < S; ++s) {
+      const int pp_s = s / P.src.tp, tp_s = s % P.src.tp;
+      uint64_t need = 0, ov = 0;
+      for (const RouteTensor& t : P.route_tensors) {
+        if (role_on(t.dst_stage, pp_d) < 0) continue;
+        const Span want = shard_span(t, tp_d, P.dst.tp);
+        need += uint64_t(want.len() * unit_elems(t));
+        if (role_on(t.src_stage, pp_s) < 0) continue;
+        const Span have = shard_span(t, tp_s, P.src.tp);
+        const Span x{std::max(have.lo, want.lo), std::min(have.hi, want.hi)};
+        ov += uint64_t(x.len() * unit_elems(t));
+      }
+      cost[size_t(d) * S + s] = (need - ov) * 14;
+    }
+  }
+  return cost;
 }
 
 void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst) {

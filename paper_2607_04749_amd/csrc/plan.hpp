@@ -20,8 +20,14 @@ RankLayout build_layout(const std::vector<LogicalTensor>& T, const Grid& g, int 
 
 // throws PlanError on bad input
 void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst);
-// layouts, routing, message layouts (host only)
+// per-tensor routing records (stages per copy role, single-copy flag)
+void build_route_tensors(etc_plan_t& P);
+// COST (D x S, bytes) on the host, for the migration sketch
+std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P);
+// layouts, routing, message layouts (host only); P.home must be set
 void build_host_plan(etc_plan_t& P);
+// migration sketch (sketch.hip): pair[i] = column paired with row i, or -1
+uint64_t solve_sketch(const uint64_t* cost, int M, int N, int32_t* pair);
 // copy descriptors of one rank (terminated by a sentinel box holding the tile count)
 std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, uint64_t* bytes);
 std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,

@@ -56,10 +56,11 @@ __host__ __device__ inline bool key_less(int role, int tp, int pp, int best_role
 }
 
 // Range of the split dim that source s sends to target d for tensor t (empty
-// when s sends nothing).  Rules (Sec. III-D with the identity pairing): data
-// that source rank d already holds stays with it (Refer); any other needed
-// element comes from its holder with the smallest key_less key.
-__host__ __device__ inline Span routed_span(const RouteTensor& t, int s, int d, int S, int TPs,
+// when s sends nothing).  home is the source rank paired with d in the
+// migration sketch (the same GPU), or -1.  Rules (Sec. III-D): data the
+// paired source already holds stays with it (Refer); any other needed element
+// comes from its holder with the smallest key_less key.
+__host__ __device__ inline Span routed_span(const RouteTensor& t, int s, int d, int home, int TPs,
                                             int TPd) {
   const Span none{0, 0};
   const int pp_d = d / TPd, tp_d = d % TPd;
@@ -71,9 +72,9 @@ __host__ __device__ inline Span routed_span(const RouteTensor& t, int s, int d, 
   const Span have = shard_span(t, tp_s, TPs);
   const Span x{have.lo > need.lo ? have.lo : need.lo, have.hi < need.hi ? have.hi : need.hi};
   if (x.len() == 0) return none;
-  if (s == d) return x;
-  if (d < S) {  // does source rank d hold this range?  Then it keeps it.
-    const int pp_x = d / TPs, tp_x = d % TPs;
+  if (s == home) return x;
+  if (home >= 0) {  // does the paired source hold this range?  Then it keeps it.
+    const int pp_x = home / TPs, tp_x = home % TPs;
     if (role_on(t.src_stage, pp_x) >= 0) {
       const Span hx = shard_span(t, tp_x, TPs);
       if (hx.lo == have.lo && hx.hi == have.hi) return none;

@@ -24,6 +24,7 @@ CM_ROUTE, CM_OVERLAP, CM_OVERLAP_SHARDED, CM_COST = 0, 1, 2, 3
 ALL_RANKS = -1
 SIDE_SRC, SIDE_DST = 0, 1
 PLAN_HOST_ONLY = 1
+PLAN_SKETCH = 2
 OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP = \
     0, -1, -2, -3, -4, -5, -6, -7
 MAX_PEERS = 128
@@ -69,8 +70,11 @@ def _load():
     L = ctypes.CDLL(LIB_PATH)
     vp, i32p, u64p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_uint64)
     L.etc_plan.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(ParallelCfg),
-                           ctypes.POINTER(ParallelCfg), ctypes.c_int, ctypes.c_uint32,
+                           ctypes.POINTER(ParallelCfg), vp, ctypes.c_int, ctypes.c_uint32,
                            ctypes.POINTER(vp)]
+    L.etc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
+    L.etc_plan_pairing.argtypes = [vp, vp]
+    L.etc_plan_process.argtypes = [vp, ctypes.c_int, i32p, i32p]
     L.etc_plan_free.argtypes = [vp]
     L.etc_plan_free.restype = None
     L.etc_plan_dims.argtypes = [vp, i32p, i32p]
@@ -189,21 +193,47 @@ class Plan:
                "etc_plan_send_layout")
         return cnt, mb, dsp, tot.value
 
+    def pairing(self):
+        """pair[d] = old rank paired with new rank d, or -1."""
+        pr = np.zeros(self.D, np.int32)
+        _check(_lib.etc_plan_pairing(self.handle, pr.ctypes.data), "etc_plan_pairing")
+        return pr
+
+    def process(self, p):
+        """(old rank, new rank) of process p, each -1 if none."""
+        a, b = ctypes.c_int(), ctypes.c_int()
+        _check(_lib.etc_plan_process(self.handle, p, ctypes.byref(a), ctypes.byref(b)),
+               "etc_plan_process")
+        return a.value, b.value
+
     def recv_counts(self, d):
         cnt = np.zeros(self.S, np.uint64)
         _check(_lib.etc_plan_recv_counts(self.handle, d, cnt.ctypes.data), "etc_plan_recv_counts")
         return cnt
 
 
-def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0):
+def etc_sketch(cost):
+    """Migration sketch of a host cost matrix (rows = new ranks): (pair, total)."""
+    c = np.ascontiguousarray(cost, np.uint64)
+    M, N = c.shape
+    pr = np.zeros(M, np.int32)
+    tot = ctypes.c_uint64()
+    _check(_lib.etc_sketch(c.ctypes.data, M, N, pr.ctypes.data, ctypes.byref(tot)), "etc_sketch")
+    return pr, tot.value
+
+
+def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None):
     """model: object with astuple() (arch, layers, hidden, heads, kv_heads, ffn,
-    vocab, max_pos, tied, flags); src/dst: objects with astuple() (tp, pp, dp)."""
+    vocab, max_pos, tied, flags); src/dst: objects with astuple() (tp, pp, dp);
+    pair: None (identity), or D entries (old rank per new rank, -1 = none)."""
     m = ModelDesc(*model.astuple())
     a = ParallelCfg(*src.astuple())
     b = ParallelCfg(*dst.astuple())
     h = ctypes.c_void_p()
-    _check(_lib.etc_plan(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), rank, flags,
-                         ctypes.byref(h)), "etc_plan")
+    pr = None if pair is None else np.ascontiguousarray(pair, np.int32)
+    _check(_lib.etc_plan(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b),
+                         None if pr is None else pr.ctypes.data, rank, flags, ctypes.byref(h)),
+           "etc_plan")
     return Plan(h, model, src, dst, rank)
 
 

@@ -77,3 +77,151 @@ def gather(buf, kind, offs):
 
 def sub(buf, byte_off, nbytes):
     return buf[byte_off:byte_off + nbytes]
+
+
+# ---- shared checks (pair: the pairing given to both the library and the oracle) ----
+
+CM = {"route": etc.CM_ROUTE, "overlap": etc.CM_OVERLAP,
+      "overlap_sharded": etc.CM_OVERLAP_SHARDED, "cost": etc.CM_COST}
+
+
+def to_dev(host):
+    return {r: [torch.from_numpy(a).to(DEV) for a in arrs] for r, arrs in host.items()}
+
+
+def device_matrices(plan):
+    S, D = plan.S, plan.D
+    out = {}
+    for name, which in CM.items():
+        buf = torch.full((S * D,), -1, dtype=torch.int64, device=DEV)
+        etc.etc_cost_matrix(plan, which, buf)
+        shape = (D, S) if name == "cost" else (S, D)
+        out[name] = buf.cpu().numpy().view(np.uint64).reshape(shape)
+    return out
+
+
+def check_matrices(plan, model, src, dst, pair=None):
+    want = oracle.matrices(model, src, dst, pair=pair)
+    got = device_matrices(plan)
+    for name in CM:
+        np.testing.assert_array_equal(got[name], want[name], err_msg=name)
+
+
+def emulate(plan, src_arenas, dst_ranks, dst_alloc):
+    """Pack every resident source, route in memory, unpack the given targets."""
+    send = {}
+    for s, ar in src_arenas.items():
+        send[s] = torch.zeros(plan.send_layout(s)[3], dtype=torch.uint8, device=DEV)
+        etc.etc_pack(plan, s, ar, send[s])
+    dst = {}
+    for d in dst_ranks:
+        msgs = []
+        for s in range(plan.S):
+            cnt, _, dsp, _ = plan.send_layout(s)
+            msgs.append(send[s].data_ptr() + int(dsp[d]) if cnt[d] else None)
+        dst[d] = dst_alloc(d)
+        etc.etc_unpack(plan, d, msgs, dst[d])
+    torch.cuda.synchronize()
+    return send, dst
+
+
+def full_compare(model, src, dst, seed, pair=None, round_trip=True):
+    """Full emulation on the GPU vs the oracle, every byte."""
+    from helpers import empty_arenas as host_empty
+    from helpers import host_arenas
+    S, D = src.world, dst.world
+    hs = host_arenas(model, src, range(S), seed)
+    hd = host_empty(model, dst, range(D))
+    hb = {s: np.zeros(oracle.send_layout(model, src, dst, s, pair=pair)[3], np.uint8) for s in range(S)}
+    oracle.migrate(model, src, dst, hs, hd, hb, pair=pair)
+    plan = etc.etc_plan(model, src, dst, pair=pair)
+    check_matrices(plan, model, src, dst, pair)
+    ds = to_dev(hs)
+    send, dd = emulate(plan, ds, range(D), lambda d: alloc(plan.arena_elems(etc.SIDE_DST, d)))
+    for s in range(S):
+        assert np.array_equal(send[s].cpu().numpy(), hb[s]), f"message buffer of source {s}"
+    for d in range(D):
+        for k in range(4):
+            assert np.array_equal(dd[d][k].cpu().numpy(), hd[d][k]), f"target {d} kind {k}"
+    if round_trip:  # A -> B -> A restores the sources
+        back_plan = etc.etc_plan(model, dst, src)
+        _, back = emulate(back_plan, dd, range(S), lambda s: alloc(back_plan.arena_elems(etc.SIDE_DST, s)))
+        for s in range(S):
+            for k in range(4):
+                assert equal(back[s][k], ds[s][k]), f"round trip source {s} kind {k}"
+
+
+def sampled_origin_check(model, src, dst, d, dst_ar, src_ars, n=4096, seed=0, pair=None):
+    elems = dst_ar[0].numel() // 2
+    rng = np.random.default_rng(seed)
+    offs = np.unique(rng.integers(0, elems, n, dtype=np.int64)).astype(np.uint64)
+    rk, so = oracle.dst_origin(model, src, dst, d, offs, pair=pair)
+    hit = rk >= 0
+    assert hit.sum() > 0
+    for k in range(4):
+        got = gather(dst_ar[k], k, offs[hit])
+        want = np.empty_like(got)
+        for s in np.unique(rk[hit]):
+            sel = rk[hit] == s
+            assert int(s) in src_ars, f"origin source {s} not resident"
+            want[sel] = gather(src_ars[int(s)][k], k, so[hit][sel])
+        np.testing.assert_array_equal(got, want, err_msg=f"target {d} kind {k}")
+
+
+def check_messages(plan, model, src, dst, s, send, src_ar, n=4096, pair=None):
+    """Sampled message elements against the oracle's serialization."""
+    cnt, mb, dsp, _ = plan.send_layout(s)
+    rng = np.random.default_rng(s)
+    for d in np.nonzero(cnt)[0]:
+        npad = int(mb[d]) // 14
+        pos = np.unique(rng.integers(0, npad, n, dtype=np.int64)).astype(np.uint64)
+        so = oracle.msg_origin(model, src, dst, s, int(d), pos, pair=pair)
+        pad = so == np.uint64(2 ** 64 - 1)
+        sec = int(dsp[d])
+        for k in range(4):
+            got = gather(send[sec:sec + npad * ESIZE[k]], k, pos)
+            want = np.zeros_like(got)
+            if (~pad).any():
+                want[~pad] = gather(src_ar[k], k, so[~pad])
+            np.testing.assert_array_equal(got, want, err_msg=f"message {s}->{d} kind {k}")
+            sec += npad * ESIZE[k]
+
+
+def expected_dst(model, cfg, d, seed):
+    ar = alloc(oracle.layout(model, cfg, d)[1])
+    fill(model, cfg, d, ar, seed)
+    return ar
+
+
+def share_run(w, plan, pair=None, check=True):
+    """Pack the share's source (and the sources feeding its target), unpack the
+    target; check messages and origins against the oracle and the whole target
+    against the seeded values."""
+    s0 = w.pack_rank
+    d0 = plan.process(w.unpack_rank)[1] if pair is not None else w.unpack_rank
+    feeders = [int(s) for s in np.nonzero(plan.recv_counts(d0))[0]]
+    resident = sorted(set(feeders) | {s0})
+    say("  resident sources", resident, "target", d0)
+    ds = seeded_arenas(w.model, w.src, resident, w.seed)
+    send = {}
+    for s in resident:
+        send[s] = torch.zeros(plan.send_layout(s)[3], dtype=torch.uint8, device=DEV)
+        etc.etc_pack(plan, s, ds[s], send[s])
+    msgs = []
+    for s in range(plan.S):
+        cnt, _, dsp, _ = plan.send_layout(s)
+        msgs.append(send[s].data_ptr() + int(dsp[d0]) if cnt[d0] else None)
+    dd = alloc(plan.arena_elems(etc.SIDE_DST, d0))
+    etc.etc_unpack(plan, d0, msgs, dd)
+    torch.cuda.synchronize()
+    if check:
+        say("  sampled messages of source", s0)
+        check_messages(plan, w.model, w.src, w.dst, s0, send[s0], ds[s0], pair=pair)
+        say("  sampled origins of target", d0)
+        sampled_origin_check(w.model, w.src, w.dst, d0, dd, ds, pair=pair)
+    del send
+    torch.cuda.empty_cache()
+    say("  full target vs seeded values")
+    exp = expected_dst(w.model, w.dst, d0, w.seed)
+    for k in range(4):
+        assert equal(dd[k], exp[k]), f"target {d0} kind {k}"
