@@ -181,7 +181,8 @@ ETC_API int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64
  * no device memory is touched.
  * On success *out owns host and device memory until etc_plan_free.
  * Errors: INVALID_ARG (also a bad pairing), INDIVISIBLE, UNSUPPORTED (dp != 1,
- * GPT with GQA), RANK, NOMEM, HIP. */
+ * GPT with GQA, a rank exchanging messages with more than ETC_MAX_PEERS peers),
+ * RANK, NOMEM, HIP. */
 ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
                      const etc_parallel_cfg* dst, const int32_t* pair, int rank, uint32_t flags,
                      etc_plan_t** out);
@@ -243,12 +244,35 @@ ETC_API int etc_pack(const etc_plan_t* plan, int src_rank, const void* const src
  * laid out as etc_pack writes it; it may be NULL when ROUTE[s][dst_rank] is 0.
  * Every payload element of the target arenas is written exactly once; bytes
  * between tensors are not touched.
- * Errors: INVALID_ARG (a needed msg[s] is NULL), RANK, ALIGN, UNSUPPORTED
- * (more than ETC_MAX_PEERS sources feed this target), HIP. */
+ * Errors: INVALID_ARG (a needed msg[s] is NULL), RANK, ALIGN, HIP. */
 ETC_API int etc_unpack(const etc_plan_t* plan, int dst_rank, const void* const* msg,
                void* const dst_arena[4], void* stream);
 
-enum { ETC_MAX_PEERS = 128 };
+enum { ETC_MAX_PEERS = 256 };
+
+/* State chunking (Sec. III-D; Sec. IV-G: one optimizer component at a time):
+ * migrate one state kind at a time through a chunk buffer that holds only
+ * that kind, so its memory can be allocated per chunk and each source arena
+ * released as soon as its kind has been packed.  Message s->d of kind k in a
+ * chunk buffer is byte for byte section k of the full message s->d.
+ * etc_plan_chunk_layout: counts[d] = bytes of message s->d for this kind
+ * (padded, 0 if nothing is routed), displs[d] = its byte offset in the chunk
+ * buffer (multiple of 256), *total = chunk buffer length.  D entries each;
+ * any output may be NULL. */
+ETC_API int etc_plan_chunk_layout(const etc_plan_t* plan, int src_rank, int kind, uint64_t* counts,
+                                  uint64_t* displs, uint64_t* total);
+
+/* Pack kind `kind` of source rank src_rank (src_arena: that kind's arena,
+ * device, read only) into chunk_buf (device, chunk layout).  Errors as
+ * etc_pack, and INVALID_ARG for a bad kind. */
+ETC_API int etc_pack_kind(const etc_plan_t* plan, int src_rank, int kind, const void* src_arena,
+                          void* chunk_buf, void* stream);
+
+/* Unpack kind `kind` into target rank dst_rank's arena of that kind; msg[s]
+ * (S entries) = message s->dst_rank in the sender's chunk layout, or NULL when
+ * nothing is routed.  Errors as etc_unpack, and INVALID_ARG for a bad kind. */
+ETC_API int etc_unpack_kind(const etc_plan_t* plan, int dst_rank, int kind, const void* const* msg,
+                            void* dst_arena, void* stream);
 
 /* Text of the calling thread's last error ("" if none).  Valid until the
  * thread's next failing call. */

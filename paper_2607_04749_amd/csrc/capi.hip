@@ -103,7 +103,7 @@ int upload(etc_plan_t* P, int rank) {
   for (int s = 0; s < S; ++s) {
     if (rank != ETC_ALL_RANKS && my_src != s) continue;
     CopyTable& t = P->pack_tab[s];
-    auto v = build_pack_boxes(*P, s, &t.bytes);
+    auto v = build_pack_boxes(*P, s, &t.peers, &t.bytes);
     t.first = uint32_t(all.size());
     t.nbox = uint32_t(v.size() - 1);
     t.ntiles = v.back().tile0;
@@ -355,10 +355,13 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
   if (!aligned(send_buf, 256)) return fail(ETC_ERR_ALIGN, "send_buf is not 256-byte aligned");
   void* arenas[4];
   for (int k = 0; k < 4; ++k) arenas[k] = const_cast<void*>(src_arena[k]);
-  void* peers[1] = {send_buf};
+  const int D = P->dst.world();
+  void* peers[ETC_MAX_PEERS];
+  for (size_t i = 0; i < t.peers.size(); ++i)
+    peers[i] = static_cast<char*>(send_buf) + P->msg_displ[size_t(s) * D + t.peers[i]];
   hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, arenas, peers, 1,
-                                  static_cast<hipStream_t>(stream));
+                                  P->copy_lds_reserve, 0xFu, true, arenas, peers,
+                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
   return ETC_OK;
 }
@@ -380,8 +383,78 @@ int etc_unpack(const etc_plan_t* P, int d, const void* const* msg, void* const d
     peers[i] = const_cast<void*>(p);
   }
   hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, dst_arena, peers, int(t.peers.size()),
-                                  static_cast<hipStream_t>(stream));
+                                  P->copy_lds_reserve, 0xFu, true, dst_arena, peers,
+                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "unpack launch");
+  return ETC_OK;
+}
+
+int etc_plan_chunk_layout(const etc_plan_t* P, int s, int kind, uint64_t* counts, uint64_t* displs,
+                          uint64_t* total) {
+  int rc = check_side_rank(P, ETC_SIDE_SRC, s);
+  if (rc) return rc;
+  if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
+  const int i = kind == ETC_KIND_PARAM_BF16 ? 0 : 1;
+  const uint64_t es = i == 0 ? 2 : 4;
+  const int D = P->dst.world();
+  for (int d = 0; d < D; ++d) {
+    const size_t sd = size_t(s) * D + d;
+    if (counts) counts[d] = P->msg_npad[sd] * es;
+    if (displs) displs[d] = P->chunk_displ[i][sd];
+  }
+  if (total) *total = P->chunk_bytes[i][s];
+  return ETC_OK;
+}
+
+int etc_pack_kind(const etc_plan_t* P, int s, int kind, const void* src_arena, void* chunk_buf,
+                  void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
+  if (s < 0 || s >= P->src.world()) return fail(ETC_ERR_RANK, "source rank out of range");
+  const etc::CopyTable& t = P->pack_tab[s];
+  if (!t.built) return fail(ETC_ERR_RANK, "source rank " + std::to_string(s) + " is not built into this plan");
+  if (!src_arena || !chunk_buf) return fail(ETC_ERR_INVALID_ARG, "src_arena and chunk_buf must not be NULL");
+  if (!aligned(src_arena, 256) || !aligned(chunk_buf, 256))
+    return fail(ETC_ERR_ALIGN, "src_arena and chunk_buf must be 256-byte aligned");
+  void* arenas[4] = {nullptr, nullptr, nullptr, nullptr};
+  arenas[kind] = const_cast<void*>(src_arena);
+  const int D = P->dst.world();
+  const int i = kind == ETC_KIND_PARAM_BF16 ? 0 : 1;
+  void* peers[ETC_MAX_PEERS];
+  for (size_t j = 0; j < t.peers.size(); ++j)
+    peers[j] = static_cast<char*>(chunk_buf) + P->chunk_displ[i][size_t(s) * D + t.peers[j]];
+  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
+                                  P->copy_lds_reserve, 1u << kind, false, arenas, peers,
+                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pack launch");
+  return ETC_OK;
+}
+
+int etc_unpack_kind(const etc_plan_t* P, int d, int kind, const void* const* msg, void* dst_arena,
+                    void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
+  if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
+  const etc::CopyTable& t = P->unpack_tab[d];
+  if (!t.built) return fail(ETC_ERR_RANK, "target rank " + std::to_string(d) + " is not built into this plan");
+  if (!dst_arena) return fail(ETC_ERR_INVALID_ARG, "dst_arena is NULL");
+  if (!aligned(dst_arena, 256)) return fail(ETC_ERR_ALIGN, "dst_arena is not 256-byte aligned");
+  if (!msg && !t.peers.empty()) return fail(ETC_ERR_INVALID_ARG, "msg is NULL");
+  void* peers[ETC_MAX_PEERS];
+  for (size_t j = 0; j < t.peers.size(); ++j) {
+    const void* p = msg[t.peers[j]];
+    if (!p) return fail(ETC_ERR_INVALID_ARG, "msg[" + std::to_string(t.peers[j]) + "] is NULL but source " +
+                                                 std::to_string(t.peers[j]) + " sends to this target");
+    if (!aligned(p, 256)) return fail(ETC_ERR_ALIGN, "msg[" + std::to_string(t.peers[j]) + "] is not 256-byte aligned");
+    peers[j] = const_cast<void*>(p);
+  }
+  void* arenas[4] = {nullptr, nullptr, nullptr, nullptr};
+  arenas[kind] = dst_arena;
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
+                                  P->copy_lds_reserve, 1u << kind, false, arenas, peers,
+                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
   return ETC_OK;
 }

@@ -32,8 +32,10 @@ struct CopyArgs {
   const CopyBox* boxes;  // nbox boxes + 1 sentinel (tile0 = ntiles)
   uint32_t nbox;
   uint32_t ntiles;
+  uint32_t kind_mask;  // kinds to copy (bit k)
+  uint32_t sectioned;  // 1: messages hold four kind sections; 0: one kind
   char* arena[4];
-  char* peer[ETC_MAX_PEERS];
+  char* peer[ETC_MAX_PEERS];  // start of each peer's message
 };
 
 constexpr int kRowBatch = 16;  // vectors in flight per thread, contiguous rows
@@ -108,7 +110,7 @@ __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox&
   constexpr int es = kKind == 0 ? 2 : 4;
   using E = typename std::conditional<es == 2, uint16_t, uint32_t>::type;
   char* A = a.arena[kKind] + tile_arena_elem(b, g) * es;
-  char* Mb = mbase + section_byte(b.msg_npad, kKind);  // this kind's section of the message
+  char* Mb = mbase + (a.sectioned ? section_byte(b.msg_npad, kKind) : 0);  // this kind's section
   char* M = Mb + tile_msg_elem(b, g) * es;
   const char* src = kPack ? A : M;
   char* dst = kPack ? M : A;
@@ -147,24 +149,26 @@ __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
       next0 = a.boxes[bi + 1].tile0;
     }
     const TileGeom g = tile_geom(b, t, next0);
-    char* mbase = a.peer[b.peer] + b.msg_byte;
-    copy_tile_kind<kPack, 0>(a, b, mbase, g);
-    copy_tile_kind<kPack, 1>(a, b, mbase, g);
-    copy_tile_kind<kPack, 2>(a, b, mbase, g);
-    copy_tile_kind<kPack, 3>(a, b, mbase, g);
+    char* mbase = a.peer[b.peer];
+    if (a.kind_mask & 1) copy_tile_kind<kPack, 0>(a, b, mbase, g);
+    if (a.kind_mask & 2) copy_tile_kind<kPack, 1>(a, b, mbase, g);
+    if (a.kind_mask & 4) copy_tile_kind<kPack, 2>(a, b, mbase, g);
+    if (a.kind_mask & 8) copy_tile_kind<kPack, 3>(a, b, mbase, g);
   }
 }
 
 }  // namespace
 
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, uint32_t lds_reserve, void* const arena[4],
-                       void* const* peers, int npeers, hipStream_t stream) {
-  if (ntiles == 0) return hipSuccess;
+                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, bool sectioned,
+                       void* const arena[4], void* const* peers, int npeers, hipStream_t stream) {
+  if (ntiles == 0 || kind_mask == 0) return hipSuccess;
   CopyArgs a{};
   a.boxes = boxes;
   a.nbox = nbox;
   a.ntiles = ntiles;
+  a.kind_mask = kind_mask;
+  a.sectioned = sectioned ? 1u : 0u;
   for (int k = 0; k < 4; ++k) a.arena[k] = static_cast<char*>(arena[k]);
   for (int p = 0; p < npeers; ++p) a.peer[p] = static_cast<char*>(peers[p]);
   const uint32_t g = grid < ntiles ? grid : ntiles;

@@ -65,12 +65,13 @@ struct RouteTensor {
 
 // One routed box between an arena (strided rows) and a message section
 // (contiguous, row-major).  Element offsets are kind-independent; the kernel
-// scales them by each kind's element size.  64 bytes.
+// scales them by each kind's element size.  The message itself is found
+// through the launch's per-peer pointer table.  64 bytes.
 struct CopyBox {
   uint64_t a_off;     // arena element offset of the box's first element
   uint64_t m_off;     // element offset inside each kind section of the message
-  uint64_t msg_byte;  // byte offset of the message from its peer base pointer
   uint64_t msg_npad;  // elements per kind section of that message
+  uint64_t reserved;
   uint32_t a_ld;      // arena row stride, elements
   uint32_t rows, cols;  // box shape; contiguous boxes are collapsed to one row
   uint32_t tr, tc;    // tile shape (rows x cols)
@@ -89,7 +90,7 @@ struct CopyTable {
   uint32_t nbox = 0;    // boxes (the array holds one more sentinel box)
   uint32_t ntiles = 0;
   uint64_t bytes = 0;   // payload bytes moved (all four kinds)
-  std::vector<int32_t> peers;  // unpack: source rank of each peer slot
+  std::vector<int32_t> peers;  // rank of each peer slot (pack: targets, unpack: sources)
 };
 
 constexpr uint32_t kTileElems = 16384;  // nominal tile: 16384 elements per kind
@@ -97,9 +98,11 @@ constexpr int kCopyThreads = 256;
 constexpr int kCmThreads = 256;
 
 // kernel launchers (copy.hip, cost.hip)
+// kind_mask: kinds to copy (bit k); sectioned: messages hold all four kind
+// sections (full format) rather than one kind (chunk format)
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, uint32_t lds_reserve, void* const arena[4],
-                       void* const* peers, int npeers, hipStream_t stream);
+                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, bool sectioned,
+                       void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
 hipError_t launch_cost(const RouteTensor* rt, int nt, const int32_t* home, int S, int D, int tps,
                        int tpd, int which, uint64_t* out, hipStream_t stream);
 
@@ -127,6 +130,11 @@ struct etc_plan_s {
   std::vector<uint64_t> msg_npad;   // padded elements per kind section
   std::vector<uint64_t> msg_displ;  // byte displacement in the sender's buffer
   std::vector<uint64_t> sendbuf_bytes;
+  // chunked migration, one state kind at a time: message s->d of a 2-byte
+  // (index 0) or 4-byte (index 1) kind at chunk_displ[i][s * D + d] in a
+  // chunk buffer of chunk_bytes[i][s] bytes
+  std::vector<uint64_t> chunk_displ[2];
+  std::vector<uint64_t> chunk_bytes[2];
 
   // device side
   int device = -1;

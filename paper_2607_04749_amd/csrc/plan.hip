@@ -179,7 +179,7 @@ void check_model(const etc_model_desc& m) {
 
 // Cut one routed box into tiles and fill its copy descriptor.
 CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint64_t m_off,
-                 uint64_t msg_byte, uint64_t msg_npad, int peer, bool pack, uint32_t tile0) {
+                 uint64_t msg_npad, int peer, bool pack, uint32_t tile0) {
   CopyBox b{};
   // a box whose rows are adjacent in the arena is one contiguous run
   if (rows == 1 || cols == a_ld) {
@@ -191,7 +191,6 @@ CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint6
     fail(ETC_ERR_UNSUPPORTED, "a routed box exceeds 2^32 elements per row");
   b.a_off = a_off;
   b.m_off = m_off;
-  b.msg_byte = msg_byte;
   b.msg_npad = msg_npad;
   b.a_ld = uint32_t(a_ld);
   b.rows = uint32_t(rows);
@@ -290,22 +289,43 @@ void build_host_plan(etc_plan_t& P) {
     }
     P.sendbuf_bytes[s] = uint64_t(round_up(int64_t(cur), 256));
   }
+  // chunk layouts: the same messages, one kind section each
+  for (int i = 0; i < 2; ++i) {
+    const uint64_t es = i == 0 ? 2 : 4;
+    P.chunk_displ[i].assign(size_t(S) * D, 0);
+    P.chunk_bytes[i].assign(S, 0);
+    for (int s = 0; s < S; ++s) {
+      uint64_t cur = 0;
+      for (int d = 0; d < D; ++d) {
+        cur = uint64_t(round_up(int64_t(cur), 256));
+        P.chunk_displ[i][size_t(s) * D + d] = cur;
+        cur += P.msg_npad[size_t(s) * D + d] * es;
+      }
+      P.chunk_bytes[i][s] = uint64_t(round_up(int64_t(cur), 256));
+    }
+  }
 }
 
-std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, uint64_t* bytes) {
+std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<int32_t>* peers,
+                                      uint64_t* bytes) {
   const int D = P.dst.world();
   std::vector<CopyBox> v;
   uint32_t tiles = 0;
   uint64_t moved = 0;
   const RankLayout& L = P.src_layout[s];
+  peers->clear();
   for (int d = 0; d < D; ++d) {
     const size_t sd = size_t(s) * D + d;
+    if (P.msg[sd].empty()) continue;
+    const int slot = int(peers->size());
+    if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "one source feeds more than ETC_MAX_PEERS targets");
+    peers->push_back(d);
     for (const auto& b : P.msg[sd]) {
       const int role_s = role_on(P.route_tensors[b.tensor].src_stage, s / P.src.tp);
       const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
       const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
-      CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_displ[sd],
-                           P.msg_npad[sd], 0, true, tiles);
+      CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
+                           true, tiles);
       const uint64_t nt = uint64_t(tiles) + box_tiles(c);
       if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
       tiles = uint32_t(nt);
@@ -337,8 +357,8 @@ std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<
     for (const auto& b : P.msg[sd]) {
       const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
       const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
-      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, 0, P.msg_npad[sd],
-                           slot, false, tiles);
+      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
+                           false, tiles);
       const uint64_t nt = uint64_t(tiles) + box_tiles(c);
       if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
       tiles = uint32_t(nt);

@@ -29,7 +29,8 @@ void build_host_plan(etc_plan_t& P);
 // migration sketch (sketch.hip): pair[i] = column paired with row i, or -1
 uint64_t solve_sketch(const uint64_t* cost, int M, int N, int32_t* pair);
 // copy descriptors of one rank (terminated by a sentinel box holding the tile count)
-std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, uint64_t* bytes);
+std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<int32_t>* peers,
+                                      uint64_t* bytes);
 std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,
                                         uint64_t* bytes);
 

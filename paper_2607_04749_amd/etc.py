@@ -27,7 +27,7 @@ PLAN_HOST_ONLY = 1
 PLAN_SKETCH = 2
 OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP = \
     0, -1, -2, -3, -4, -5, -6, -7
-MAX_PEERS = 128
+MAX_PEERS = 256
 ESIZE = (2, 4, 4, 4)
 
 
@@ -88,6 +88,9 @@ def _load():
     L.etc_cost_matrix.argtypes = [vp, ctypes.c_int, vp, vp]
     L.etc_pack.argtypes = [vp, ctypes.c_int, vp, vp, vp]
     L.etc_unpack.argtypes = [vp, ctypes.c_int, vp, vp, vp]
+    L.etc_plan_chunk_layout.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, u64p]
+    L.etc_pack_kind.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, vp]
+    L.etc_unpack_kind.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, vp]
     L.etc_last_error.argtypes = []
     L.etc_last_error.restype = ctypes.c_char_p
     if len(hip_runtimes()) > 1:
@@ -206,6 +209,15 @@ class Plan:
                "etc_plan_process")
         return a.value, b.value
 
+    def chunk_layout(self, s, kind):
+        """(counts, displs, total) of source s's chunk buffer for one state kind."""
+        cnt = np.zeros(self.D, np.uint64)
+        dsp = np.zeros(self.D, np.uint64)
+        tot = ctypes.c_uint64()
+        _check(_lib.etc_plan_chunk_layout(self.handle, s, kind, cnt.ctypes.data, dsp.ctypes.data,
+                                          ctypes.byref(tot)), "etc_plan_chunk_layout")
+        return cnt, dsp, tot.value
+
     def recv_counts(self, d):
         cnt = np.zeros(self.S, np.uint64)
         _check(_lib.etc_plan_recv_counts(self.handle, d, cnt.ctypes.data), "etc_plan_recv_counts")
@@ -256,3 +268,17 @@ def etc_unpack(plan, dst_rank, msgs, dst_arenas, stream=None):
     arr = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
     _check(_lib.etc_unpack(plan.handle, dst_rank, ctypes.cast(m, ctypes.c_void_p),
                            ctypes.cast(arr, ctypes.c_void_p), _stream(stream)), "etc_unpack")
+
+
+def etc_pack_kind(plan, src_rank, kind, src_arena, chunk_buf, stream=None):
+    _check(_lib.etc_pack_kind(plan.handle, src_rank, kind, _ptr(src_arena), _ptr(chunk_buf),
+                              _stream(stream)), "etc_pack_kind")
+
+
+def etc_unpack_kind(plan, dst_rank, kind, msgs, dst_arena, stream=None):
+    """msgs: S entries (tensor, int pointer or None), each in the chunk layout."""
+    if len(msgs) != plan.S:
+        raise ValueError(f"need {plan.S} message pointers, got {len(msgs)}")
+    m = (ctypes.c_void_p * plan.S)(*[_ptr(x) for x in msgs])
+    _check(_lib.etc_unpack_kind(plan.handle, dst_rank, kind, ctypes.cast(m, ctypes.c_void_p),
+                                _ptr(dst_arena), _stream(stream)), "etc_unpack_kind")

@@ -125,3 +125,36 @@ def test_rank_plan_send_layout_any_source():
     p = etc.etc_plan(w.model, w.src, w.dst, rank=0, flags=HOST)
     for s in range(w.src.world):
         np.testing.assert_array_equal(p.send_layout(s)[0], oracle.send_layout(w.model, w.src, w.dst, s)[0])
+
+
+@pytest.mark.parametrize("wl", sorted(WORKLOADS))
+def test_chunk_layout(wl):
+    """Chunked migration (one state kind at a time): message s->d of kind k in
+    a chunk buffer has the length of section k of the full message; messages
+    sit in target order at multiples of 256 bytes."""
+    w = WORKLOADS[wl]
+    p = etc.etc_plan(w.model, w.src, w.dst, flags=HOST)
+    for s in range(min(w.src.world, 4)):
+        cnt, mb, dsp, tot = p.send_layout(s)
+        for k, es in enumerate((2, 4, 4, 4)):
+            c, d, t = p.chunk_layout(s, k)
+            np.testing.assert_array_equal(c, mb // 14 * es)
+            assert (d % 256 == 0).all()
+            end = 0
+            for dd in range(w.dst.world):
+                assert d[dd] >= end
+                end = int(d[dd]) + int(c[dd])
+            assert t >= end and t % 256 == 0
+    with pytest.raises(etc.EtcError) as e:
+        p.chunk_layout(0, 4)
+    assert e.value.code == etc.ERR_INVALID_ARG
+
+
+def test_chunk_calls_need_device_plan():
+    w = WORKLOADS["tiny-gpt"]
+    p = etc.etc_plan(w.model, w.src, w.dst, flags=HOST)
+    for call in (lambda: etc.etc_pack_kind(p, 0, 1, 0, 0, stream=0),
+                 lambda: etc.etc_unpack_kind(p, 0, 1, [None] * 4, 0, stream=0)):
+        with pytest.raises(etc.EtcError) as e:
+            call()
+        assert e.value.code == etc.ERR_INVALID_ARG
