@@ -27,7 +27,11 @@
  * send/recv or all-to-all-v with the counts from etc_plan_send_layout).
  *
  * Conventions shared by all calls
- *   Ranks.   rank = pp * TP + tp (TP fastest); data parallel must be 1.
+ *   Ranks.   rank = dp * (PP * TP) + pp * TP + tp: TP fastest, then PP; each
+ *            data-parallel replica is a contiguous block of ranks.  Target
+ *            replica j is served by source replica j mod DP_src (replicas that
+ *            are kept stay, new replicas are fed round-robin; Sec. III-C), and
+ *            a failed source's data comes from the next live replica.
  *   Layers.  Stage p holds layers [p*L/PP, (p+1)*L/PP); the embedding (and a
  *            GPT position table) sits on the first stage; the final norm and
  *            the output head on the last.  A tied embedding also has a
@@ -96,7 +100,11 @@ enum { ETC_KIND_PARAM_BF16 = 0, ETC_KIND_MASTER_F32 = 1, ETC_KIND_ADAM_M_F32 = 2
  *                   configurations.
  *  COST             D x S: the paper's cost matrix c_ij (rows are the new
  *                   ranks, columns the old ranks, Sec. III-B):
- *                   bytes(d) - OVERLAP[s][d]. */
+ *                   bytes(d) - OVERLAP[s][d]; ETC_COST_INF between
+ *                   different data-parallel replicas and towards failed
+ *                   ranks.  A failed rank holds nothing.  OVERLAP_SHARDED
+ *                   counts tensors with one copy per replica, and only when
+ *                   s lies in the replica serving d. */
 enum { ETC_CM_ROUTE = 0, ETC_CM_OVERLAP = 1, ETC_CM_OVERLAP_SHARDED = 2, ETC_CM_COST = 3 };
 
 enum { ETC_ALL_RANKS = -1 };
@@ -117,8 +125,13 @@ enum {
   ETC_ERR_ALIGN = -4,       /* a device pointer is not 256-byte aligned           */
   ETC_ERR_UNSUPPORTED = -5, /* dp != 1, too many peers, or a size limit exceeded  */
   ETC_ERR_NOMEM = -6,       /* host or device allocation failed (etc_plan only)   */
-  ETC_ERR_HIP = -7          /* a HIP runtime call failed; see etc_last_error()    */
+  ETC_ERR_HIP = -7,         /* a HIP runtime call failed; see etc_last_error()    */
+  ETC_ERR_UNRECOVERABLE = -8 /* needed data survives on no live source rank      */
 };
+
+/* COST between ranks of different data-parallel replicas, or towards a
+ * failed rank: the paper's "infinite" workload difference (Sec. III-C). */
+#define ETC_COST_INF (1ull << 50)
 
 typedef struct {
   int32_t arch;            /* ETC_ARCH_*                                  */
@@ -134,7 +147,7 @@ typedef struct {
 } etc_model_desc;
 
 typedef struct {
-  int32_t tp, pp, dp; /* dp must be 1 */
+  int32_t tp, pp, dp;
 } etc_parallel_cfg;
 
 typedef struct etc_plan_s etc_plan_t;
@@ -163,29 +176,42 @@ typedef struct {
  * Errors: INVALID_ARG, UNSUPPORTED, NOMEM. */
 ETC_API int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* total);
 
+/* Options of etc_plan (NULL = all defaults: identity pairing, no failures,
+ * every rank, no flags). */
+typedef struct {
+  const int32_t* pair;   /* D entries, host: pair[d] = the old rank whose GPU
+                            becomes new rank d, or -1 for a new GPU; each old
+                            rank at most once, never across data-parallel
+                            replicas or with a failed rank.  NULL: identity
+                            pairing (d with d, where both lie in the same
+                            replica and d is alive), or the optimal sketch
+                            with ETC_PLAN_SKETCH */
+  const int32_t* failed; /* old ranks whose states are lost (host), or NULL */
+  int32_t num_failed;
+  int32_t rank;          /* process to build device tables for, or ETC_ALL_RANKS */
+  uint32_t flags;        /* ETC_PLAN_* */
+} etc_plan_options;
+
 /* Build a migration plan from `model`, the old configuration `src` and the new
  * configuration `dst` (Sec. III: the primitive's inputs are the two parallel
- * configurations and the model), with new ranks paired to old ranks by
- * `pair` (D entries, host: pair[d] = the old rank whose GPU becomes new rank
- * d, or -1 for a new GPU; each old rank at most once), or by the identity
- * pairing when pair is NULL, or by the optimal sketch with ETC_PLAN_SKETCH.
- * Host work: the logical tensor table, every rank's layout, the routing of
- * every target element, every message layout.
- * `rank` names a process: process p < S holds old rank p and becomes the new
- * rank paired with it (if any); processes S, S+1, ... are new GPUs and take
- * the unpaired new ranks in ascending order (etc_plan_process reports both
- * roles).  Device tables (routed boxes cut into uniform tiles, the tensor
- * table and the pairing for etc_cost_matrix) are built for that process's
- * pack and unpack, or for every rank with ETC_ALL_RANKS, and copied to the
- * current device, which the plan is then bound to.  With ETC_PLAN_HOST_ONLY
- * no device memory is touched.
+ * configurations and the model), with new ranks paired to old ranks as
+ * opt->pair says.  Host work: the logical tensor table, every rank's layout,
+ * the routing of every target element, every message layout.
+ * opt->rank names a process: process p < S holds old rank p and becomes the
+ * new rank paired with it (if any); processes S, S+1, ... are new GPUs and
+ * take the unpaired new ranks in ascending order (etc_plan_process reports
+ * both roles).  Device tables (routed boxes cut into uniform tiles, the tensor
+ * table, the pairing and the failed ranks for etc_cost_matrix) are built for
+ * that process's pack and unpack, or for every rank with ETC_ALL_RANKS, and
+ * copied to the current device, which the plan is then bound to.  With
+ * ETC_PLAN_HOST_ONLY no device memory is touched.
  * On success *out owns host and device memory until etc_plan_free.
- * Errors: INVALID_ARG (also a bad pairing), INDIVISIBLE, UNSUPPORTED (dp != 1,
- * GPT with GQA, a rank exchanging messages with more than ETC_MAX_PEERS peers),
- * RANK, NOMEM, HIP. */
+ * Errors: INVALID_ARG (also a bad pairing or failed list), INDIVISIBLE,
+ * UNSUPPORTED (GPT with GQA, more than 65536 ranks, a rank exchanging messages
+ * with more than ETC_MAX_PEERS peers), UNRECOVERABLE (every replica of some
+ * needed data failed), RANK, NOMEM, HIP. */
 ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
-                     const etc_parallel_cfg* dst, const int32_t* pair, int rank, uint32_t flags,
-                     etc_plan_t** out);
+                     const etc_parallel_cfg* dst, const etc_plan_options* opt, etc_plan_t** out);
 
 /* The plan's pairing: pair[d] (D entries) = old rank paired with new rank d, or -1. */
 ETC_API int etc_plan_pairing(const etc_plan_t* plan, int32_t* pair);

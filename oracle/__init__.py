@@ -20,6 +20,8 @@ SRC_PATH = os.path.join(_HERE, "oracle.c")
 OK = 0
 EINVAL, EINDIV, ERANK, EUNSUP, ENOMEM = -1, -2, -3, -5, -6
 EMISMATCH, EUNCOVERED, EBOX = -10, -11, -12
+EUNRECOVERABLE = -8
+COST_INF = 1 << 50
 ESIZE = (2, 4, 4, 4)
 BYTES_PER_ELEM = 14
 MSG_ALIGN = 256
@@ -60,6 +62,11 @@ class MBox(ctypes.Structure):
     _fields_ = [("tensor", ctypes.c_int32), ("role_d", ctypes.c_int32), ("r0", ctypes.c_int64),
                 ("r1", ctypes.c_int64), ("c0", ctypes.c_int64), ("c1", ctypes.c_int64),
                 ("moff", ctypes.c_uint64)]
+
+
+class Route(ctypes.Structure):
+    _fields_ = [("pair", ctypes.c_void_p), ("failed", ctypes.c_void_p),
+                ("num_failed", ctypes.c_int32)]
 
 
 class OracleError(RuntimeError):
@@ -113,13 +120,15 @@ def _ptr(a):
     return ctypes.c_void_p(a.ctypes.data) if a is not None else ctypes.c_void_p(0)
 
 
-def _pair(pair):
-    """Pairing (new rank -> old rank or -1) as an int32 array, or None for the
-    identity pairing.  Keeps the array alive with the returned pointer."""
-    if pair is None:
+def _route(pair, failed):
+    """orc_route for a pairing (new rank -> old rank or -1; None = identity)
+    and a list of failed old ranks.  Returns (keep-alive, pointer)."""
+    if pair is None and not failed:
         return None, ctypes.c_void_p(0)
-    a = np.ascontiguousarray(pair, np.int32)
-    return a, ctypes.c_void_p(a.ctypes.data)
+    pa = None if pair is None else np.ascontiguousarray(pair, np.int32)
+    fa = np.ascontiguousarray(failed if failed else [0], np.int32)
+    r = Route(None if pa is None else pa.ctypes.data, fa.ctypes.data, len(failed) if failed else 0)
+    return (pa, fa, r), ctypes.cast(ctypes.pointer(r), ctypes.c_void_p)
 
 
 def tensors(model):
@@ -148,7 +157,7 @@ def layout(model, cfg, rank):
             for p in arr[:n]], elems.value
 
 
-def matrices(model, src, dst, brute=False, pair=None):
+def matrices(model, src, dst, brute=False, pair=None, failed=None):
     """dict route (SxD), overlap (SxD), overlap_sharded (SxD), cost (DxS), bytes."""
     S, D = src.world, dst.world
     r = np.zeros((S, D), np.uint64)
@@ -157,13 +166,13 @@ def matrices(model, src, dst, brute=False, pair=None):
     cst = np.zeros((D, S), np.uint64)
     f = lib().orc_matrices_bruteforce if brute else lib().orc_matrices
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _pair(pair)
+    keep, pp = _route(pair, failed)
     _check(f(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, _ptr(r), _ptr(o), _ptr(osh),
              _ptr(cst)), "matrices")
     return dict(route=r, overlap=o, overlap_sharded=osh, cost=cst)
 
 
-def send_layout(model, src, dst, s, pair=None):
+def send_layout(model, src, dst, s, pair=None, failed=None):
     """(counts, padded, displs, total) in bytes for source s."""
     D = dst.world
     cnt = np.zeros(D, np.uint64)
@@ -171,17 +180,17 @@ def send_layout(model, src, dst, s, pair=None):
     dsp = np.zeros(D, np.uint64)
     tot = ctypes.c_uint64()
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _pair(pair)
+    keep, pp = _route(pair, failed)
     _check(lib().orc_send_layout(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s,
                                  _ptr(cnt), _ptr(pad), _ptr(dsp), ctypes.byref(tot)), "send_layout")
     return cnt, pad, dsp, tot.value
 
 
-def message(model, src, dst, s, d, pair=None):
+def message(model, src, dst, s, d, pair=None, failed=None):
     """(boxes, npad): the boxes of message s->d in order, and the section length."""
     m, a, b = _m(model), _c(src), _c(dst)
     npad = ctypes.c_uint64()
-    keep, pp = _pair(pair)
+    keep, pp = _route(pair, failed)
     n = _check(lib().orc_message(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d, None,
                                  0, ctypes.byref(npad)), "message")
     arr = (MBox * max(n, 1))()
@@ -192,7 +201,7 @@ def message(model, src, dst, s, d, pair=None):
 
 
 def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0, t_hi=-1,
-            pair=None):
+            pair=None, failed=None):
     """Materialize-then-reslice.  src_arenas: {rank: [4 uint8 arrays]} (resident
     sources); dst_arenas: {rank: [4 uint8 arrays]} to fill; send_bufs:
     {rank: uint8 array} to fill with that source's messages."""
@@ -209,31 +218,31 @@ def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0
     for s, arr in (send_bufs or {}).items():
         sb[s] = arr.ctypes.data
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _pair(pair)
+    keep, pp = _route(pair, failed)
     _check(lib().orc_migrate(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp,
                              ctypes.cast(sa, ctypes.c_void_p), ctypes.cast(da, ctypes.c_void_p),
                              ctypes.cast(sb, ctypes.c_void_p), t_lo, t_hi), "migrate")
 
 
-def dst_origin(model, src, dst, d, offs, pair=None):
+def dst_origin(model, src, dst, d, offs, pair=None, failed=None):
     """(src_rank int32[n], src_off uint64[n]) for destination arena element offsets."""
     offs = np.ascontiguousarray(offs, np.uint64)
     rk = np.zeros(offs.size, np.int32)
     so = np.zeros(offs.size, np.uint64)
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _pair(pair)
+    keep, pp = _route(pair, failed)
     _check(lib().orc_dst_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, d,
                                 _ptr(offs), offs.size, _ptr(rk), _ptr(so)), "dst_origin")
     return rk, so
 
 
-def msg_origin(model, src, dst, s, d, pos, pair=None):
+def msg_origin(model, src, dst, s, d, pos, pair=None, failed=None):
     """Source-arena element offsets for element positions inside a kind section
     of message s->d (UINT64_MAX for padding)."""
     pos = np.ascontiguousarray(pos, np.uint64)
     so = np.zeros(pos.size, np.uint64)
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _pair(pair)
+    keep, pp = _route(pair, failed)
     _check(lib().orc_msg_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d,
                                 _ptr(pos), pos.size, _ptr(so)), "msg_origin")
     return so

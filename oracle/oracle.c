@@ -58,6 +58,11 @@
 #define ORC_EMISMATCH -10 /* replicas disagree                          */
 #define ORC_EUNCOVERED -11 /* a needed element is held by no resident source */
 #define ORC_EBOX -12 /* routed elements do not form one box          */
+#define ORC_EUNRECOVERABLE -8 /* a needed element survives on no source rank */
+
+/* cost between ranks of different data-parallel replicas (Sec. III-C: the
+ * workload difference across DP ranks is taken as infinite) */
+#define ORC_COST_INF ((uint64_t)1 << 50)
 
 #define ORC_NKIND 4
 #define ORC_ALIGN_ELEMS 128
@@ -76,6 +81,15 @@ typedef struct {
 typedef struct {
   int32_t tp, pp, dp;
 } orc_cfg;
+
+/* Routing inputs beyond the two configurations: the migration sketch
+ * (pair[d] = old rank paired with new rank d, or -1; NULL = identity) and the
+ * old ranks whose states are lost (failed[0..num_failed)). */
+typedef struct {
+  const int32_t* pair;
+  const int32_t* failed;
+  int32_t num_failed;
+} orc_route;
 
 typedef struct {
   char name[48];
@@ -192,8 +206,7 @@ static int build_tensors(const orc_model* m, orc_tensor* out) {
  * divide TP (Sec. IV-A, models paragraph).  Every other dim that TP splits
  * must divide too, and a QKV shard must hold whole KV groups. */
 static int check_cfg(const orc_model* m, const orc_cfg* c) {
-  if (c->tp < 1 || c->pp < 1) return ORC_EINVAL;
-  if (c->dp != 1) return ORC_EUNSUP;
+  if (c->tp < 1 || c->pp < 1 || c->dp < 1) return ORC_EINVAL;
   if (m->num_layers % c->pp) return ORC_EINDIV;
   if (m->hidden % c->tp || m->ffn_hidden % c->tp) return ORC_EINDIV;
   if (m->num_kv_heads % c->tp) return ORC_EINDIV;
@@ -246,11 +259,15 @@ static void box_of(const orc_tensor* t, int tp, int TP, int64_t* r0, int64_t* r1
 
 static int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
-/* Rank = pp * TP + tp (Megatron order, TP fastest; DP = 1). */
+/* Rank = dp * (PP * TP) + pp * TP + tp: TP fastest, then PP, each data-
+ * parallel replica a contiguous block of ranks. */
 static void coords(const orc_cfg* c, int rank, int* pp, int* tp) {
-  *pp = rank / c->tp;
-  *tp = rank % c->tp;
+  const int in_replica = rank % (c->pp * c->tp);
+  *pp = in_replica / c->tp;
+  *tp = in_replica % c->tp;
 }
+
+static int replica_of(const orc_cfg* c, int rank) { return rank / (c->pp * c->tp); }
 
 /* A rank's arena: role-0 pieces in tensor order, then role-1 pieces.  Each
  * local tensor starts at a multiple of 128 elements; a fused tensor (up after
@@ -293,7 +310,8 @@ typedef struct {
   orc_model m;
   orc_cfg src, dst;
   int S, D, nt;
-  int32_t* home; /* home[d]: source rank paired with target d (the same GPU), or -1 */
+  int32_t* home;  /* home[d]: source rank paired with target d (the same GPU), or -1 */
+  char* failed;   /* failed[s]: source rank s lost its states */
   orc_tensor* T;
   int* ns;           /* pieces per source rank      */
   orc_piece** ps;    /* pieces of each source rank  */
@@ -315,13 +333,17 @@ static void ctx_free(ctx_t* x) {
   free(x->d_elems);
   free(x->T);
   free(x->home);
+  free(x->failed);
   memset(x, 0, sizeof *x);
 }
 
-/* pair: pair[d] = source rank paired with target d, or -1 (a migration sketch,
- * Sec. III-B); NULL means the identity pairing (target d with source d). */
+/* route: pairing and failed ranks (NULL = identity pairing, no failures).
+ * Under the identity pairing target d pairs with source d when both exist
+ * and source d is alive.  A pairing may only join ranks of the same data-
+ * parallel replica, and never a failed rank. */
 static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_cfg* dst,
-                    const int32_t* pair) {
+                    const orc_route* route) {
+  const int32_t* pair = route ? route->pair : NULL;
   memset(x, 0, sizeof *x);
   int rc = check_model(m);
   if (rc) return rc;
@@ -330,8 +352,8 @@ static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_
   x->m = *m;
   x->src = *src;
   x->dst = *dst;
-  x->S = src->tp * src->pp;
-  x->D = dst->tp * dst->pp;
+  x->S = src->tp * src->pp * src->dp;
+  x->D = dst->tp * dst->pp * dst->dp;
   x->nt = build_tensors(m, NULL);
   x->T = calloc((size_t)x->nt, sizeof(orc_tensor));
   x->ns = calloc((size_t)x->S, sizeof(int));
@@ -346,13 +368,31 @@ static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_
   }
   build_tensors(m, x->T);
   x->home = calloc((size_t)x->D, sizeof(int32_t));
-  if (!x->home) {
+  x->failed = calloc((size_t)x->S, 1);
+  if (!x->home || !x->failed) {
     ctx_free(x);
     return ORC_ENOMEM;
   }
+  for (int i = 0; route && i < route->num_failed; ++i) {
+    if (route->failed[i] < 0 || route->failed[i] >= x->S) {
+      ctx_free(x);
+      return ORC_EINVAL;
+    }
+    x->failed[route->failed[i]] = 1;
+  }
   for (int d = 0; d < x->D; ++d) {
-    x->home[d] = pair ? pair[d] : (d < x->S ? d : -1);
+    if (pair) {
+      x->home[d] = pair[d];
+    } else {
+      x->home[d] = -1;
+      if (d < x->S && !x->failed[d] && replica_of(src, d) == replica_of(dst, d)) x->home[d] = d;
+    }
     if (x->home[d] < -1 || x->home[d] >= x->S) {
+      ctx_free(x);
+      return ORC_EINVAL;
+    }
+    if (x->home[d] >= 0 &&
+        (x->failed[x->home[d]] || replica_of(src, x->home[d]) != replica_of(dst, d))) {
       ctx_free(x);
       return ORC_EINVAL;
     }
@@ -407,29 +447,39 @@ static int sender_of_element(const ctx_t* x, int d, int role_d, int t, int64_t r
   }
   int pp_d, tp_d;
   coords(&x->dst, d, &pp_d, &tp_d);
-  int best = -1;
-  int bk[4] = {0, 0, 0, 0};
-  for (int s = 0; s < x->S; ++s) {
-    for (int i = 0; i < x->ns[s]; ++i) {
-      const orc_piece* p = &x->ps[s][i];
-      if (p->tensor != t || !in_box(p, r, c)) continue;
-      int pp_s, tp_s;
-      coords(&x->src, s, &pp_s, &tp_s);
-      int k[4] = {p->role != role_d, tp_s != tp_d % x->src.tp, pp_s, tp_s};
-      int less = best < 0;
-      for (int j = 0; j < 4 && !less; ++j) {
-        if (k[j] != bk[j]) {
-          less = k[j] < bk[j];
-          break;
+  /* data-parallel isolation: target replica j is served by source replica
+   * j mod DP_src (kept replicas stay, scale-out replicas round-robin); if no
+   * live rank of that replica holds the element, the next replicas in order
+   * stand in for it (fault tolerance through DP replicas, Sec. III-C) */
+  const int r0 = replica_of(&x->dst, d) % x->src.dp;
+  for (int step = 0; step < x->src.dp; ++step) {
+    const int rep = (r0 + step) % x->src.dp;
+    int best = -1;
+    int bk[4] = {0, 0, 0, 0};
+    for (int s = 0; s < x->S; ++s) {
+      if (x->failed[s] || replica_of(&x->src, s) != rep) continue;
+      for (int i = 0; i < x->ns[s]; ++i) {
+        const orc_piece* p = &x->ps[s][i];
+        if (p->tensor != t || !in_box(p, r, c)) continue;
+        int pp_s, tp_s;
+        coords(&x->src, s, &pp_s, &tp_s);
+        int k[4] = {p->role != role_d, tp_s != tp_d % x->src.tp, pp_s, tp_s};
+        int less = best < 0;
+        for (int j = 0; j < 4 && !less; ++j) {
+          if (k[j] != bk[j]) {
+            less = k[j] < bk[j];
+            break;
+          }
+        }
+        if (less) {
+          best = s;
+          memcpy(bk, k, sizeof k);
         }
       }
-      if (less) {
-        best = s;
-        memcpy(bk, k, sizeof k);
-      }
     }
+    if (best >= 0) return best;
   }
-  return best;
+  return -1;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -473,31 +523,38 @@ static int sender_of_item(const ctx_t* x, int d, int role_d, const orc_tensor* t
   }
   int pp_d, tp_d;
   coords(&x->dst, d, &pp_d, &tp_d);
-  int best = -1;
-  int bk[4] = {0, 0, 0, 0};
-  for (int s = 0; s < x->S; ++s) {
-    int pp_s, tp_s;
-    coords(&x->src, s, &pp_s, &tp_s);
-    for (int role = 0; role < 2; ++role) {
-      if (!holds_item(x, &x->src, pp_s, tp_s, t, role, a)) continue;
-      int k[4] = {role != role_d, tp_s != tp_d % x->src.tp, pp_s, tp_s};
-      int less = best < 0;
-      for (int j = 0; j < 4 && !less; ++j) {
-        if (k[j] != bk[j]) {
-          less = k[j] < bk[j];
-          break;
+  const int r0 = replica_of(&x->dst, d) % x->src.dp;
+  for (int step = 0; step < x->src.dp; ++step) {
+    const int rep = (r0 + step) % x->src.dp;
+    int best = -1;
+    int bk[4] = {0, 0, 0, 0};
+    for (int s = 0; s < x->S; ++s) {
+      if (x->failed[s] || replica_of(&x->src, s) != rep) continue;
+      int pp_s, tp_s;
+      coords(&x->src, s, &pp_s, &tp_s);
+      for (int role = 0; role < 2; ++role) {
+        if (!holds_item(x, &x->src, pp_s, tp_s, t, role, a)) continue;
+        int k[4] = {role != role_d, tp_s != tp_d % x->src.tp, pp_s, tp_s};
+        int less = best < 0;
+        for (int j = 0; j < 4 && !less; ++j) {
+          if (k[j] != bk[j]) {
+            less = k[j] < bk[j];
+            break;
+          }
+        }
+        if (less) {
+          best = s;
+          memcpy(bk, k, sizeof k);
         }
       }
-      if (less) {
-        best = s;
-        memcpy(bk, k, sizeof k);
-      }
     }
+    if (best >= 0) return best;
   }
-  return best;
+  return -1;
 }
 
-/* Copies of a tensor in a configuration: copy roles times TP ranks holding it. */
+/* Copies of a tensor inside one data-parallel replica of a configuration:
+ * copy roles times TP ranks holding it. */
 static int multiplicity(const ctx_t* x, const orc_cfg* c, const orc_tensor* t) {
   int roles = (stage_of(&x->m, c, t, 0) >= 0) + (stage_of(&x->m, c, t, 1) >= 0);
   return roles * (t->split == ORC_REPL ? c->tp : 1);
@@ -531,7 +588,7 @@ int orc_layout(const orc_model* m, const orc_cfg* c, int rank, orc_piece* out, i
   int rc = check_model(m);
   if (rc) return rc;
   if ((rc = check_cfg(m, c))) return rc;
-  if (rank < 0 || rank >= c->tp * c->pp) return ORC_ERANK;
+  if (rank < 0 || rank >= c->tp * c->pp * c->dp) return ORC_ERANK;
   int nt = build_tensors(m, NULL);
   orc_tensor* T = calloc((size_t)nt, sizeof *T);
   if (!T) return ORC_ENOMEM;
@@ -555,15 +612,18 @@ int orc_layout(const orc_model* m, const orc_cfg* c, int rank, orc_piece* out, i
 /* ROUTE[s][d]: bytes source s sends to destination d under the sender rule.
  * OVERLAP[s][d]: bytes of (held by s) intersect (needed by d), intersecting
  *   logical identities (tensor, element), so a replica counts as held.
- * OVERLAP_SHARDED[s][d]: OVERLAP over tensors with exactly one copy in both
- *   configurations.
+ * OVERLAP_SHARDED[s][d]: OVERLAP over tensors with exactly one copy per
+ *   data-parallel replica in both configurations, counted only when s lies in
+ *   the source replica serving d.
  * COST[d][s] = bytes(d) - OVERLAP[s][d]: the paper's c_ij with rows = the new
- *   (curr) ranks and columns = the old (prev) ranks (Sec. III-B), in bytes.
+ *   (curr) ranks and columns = the old (prev) ranks (Sec. III-B), in bytes;
+ *   ORC_COST_INF when s and d lie in different data-parallel replicas or s
+ *   failed (Sec. III-C).  A failed rank holds nothing.
  * Computed over LCM workload items (Sec. III-C).  Any output may be NULL. */
-int orc_matrices(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
-                 uint64_t* route, uint64_t* overlap, uint64_t* overlap_sh, uint64_t* cost) {
+int orc_matrices(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const orc_route* route,
+                 uint64_t* route_m, uint64_t* overlap, uint64_t* overlap_sh, uint64_t* cost) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   const int S = x.S, D = x.D;
   uint64_t* R = calloc((size_t)S * D, 8);
@@ -583,22 +643,24 @@ int orc_matrices(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, con
     for (int d = 0; d < D; ++d) {
       int pp_d, tp_d;
       coords(dst, d, &pp_d, &tp_d);
+      const int serving = replica_of(dst, d) % src->dp; /* source replica serving d */
       for (int role_d = 0; role_d < 2; ++role_d) {
         for (int64_t a = 0; a < G; ++a) {
           if (!holds_item(&x, dst, pp_d, tp_d, t, role_d, a)) continue;
           need[d] += item_bytes;
           for (int s = 0; s < S; ++s) {
+            if (x.failed[s]) continue; /* a failed rank holds nothing */
             int pp_s, tp_s;
             coords(src, s, &pp_s, &tp_s);
             if (holds_item(&x, src, pp_s, tp_s, t, 0, a) ||
                 holds_item(&x, src, pp_s, tp_s, t, 1, a)) {
               O[(size_t)s * D + d] += item_bytes;
-              if (sharded) OS[(size_t)s * D + d] += item_bytes;
+              if (sharded && replica_of(src, s) == serving) OS[(size_t)s * D + d] += item_bytes;
             }
           }
           int snd = sender_of_item(&x, d, role_d, t, a);
           if (snd < 0) {
-            rc = ORC_EUNCOVERED;
+            rc = ORC_EUNRECOVERABLE;
             goto out;
           }
           R[(size_t)snd * D + d] += item_bytes;
@@ -606,12 +668,16 @@ int orc_matrices(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, con
       }
     }
   }
-  if (route) memcpy(route, R, (size_t)S * D * 8);
+  if (route_m) memcpy(route_m, R, (size_t)S * D * 8);
   if (overlap) memcpy(overlap, O, (size_t)S * D * 8);
   if (overlap_sh) memcpy(overlap_sh, OS, (size_t)S * D * 8);
   if (cost)
     for (int d = 0; d < D; ++d)
-      for (int s = 0; s < S; ++s) cost[(size_t)d * S + s] = need[d] - O[(size_t)s * D + d];
+      for (int s = 0; s < S; ++s)
+        cost[(size_t)d * S + s] =
+            (x.failed[s] || replica_of(src, s) != replica_of(dst, d))
+                ? ORC_COST_INF
+                : need[d] - O[(size_t)s * D + d];
 out:
   free(R); free(O); free(OS); free(need);
   ctx_free(&x);
@@ -621,10 +687,10 @@ out:
 /* The same four matrices by enumerating every element of every tensor and
  * scanning every rank's pieces for it.  Tiny models only. */
 int orc_matrices_bruteforce(const orc_model* m, const orc_cfg* src, const orc_cfg* dst,
-                            const int32_t* pair, uint64_t* route, uint64_t* overlap,
+                            const orc_route* route, uint64_t* route_m, uint64_t* overlap,
                             uint64_t* overlap_sh, uint64_t* cost) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   const int S = x.S, D = x.D;
   uint64_t* R = calloc((size_t)S * D, 8);
@@ -641,31 +707,34 @@ int orc_matrices_bruteforce(const orc_model* m, const orc_cfg* src, const orc_cf
     const orc_tensor* t = &x.T[ti];
     for (int64_t r = 0; r < t->rows; ++r) {
       for (int64_t c = 0; c < t->cols; ++c) {
-        int cs = 0, cd = 0;
+        int cs = 0, cd = 0; /* copies of the element in the whole configurations */
         for (int s = 0; s < S; ++s)
           for (int i = 0; i < x.ns[s]; ++i)
             if (x.ps[s][i].tensor == ti && in_box(&x.ps[s][i], r, c)) ++cs;
         for (int d = 0; d < D; ++d)
           for (int i = 0; i < x.nd[d]; ++i)
             if (x.pd[d][i].tensor == ti && in_box(&x.pd[d][i], r, c)) ++cd;
-        const int sharded = cs == 1 && cd == 1;
+        /* one copy per data-parallel replica on both sides */
+        const int sharded = cs == src->dp && cd == dst->dp;
         for (int d = 0; d < D; ++d) {
           for (int i = 0; i < x.nd[d]; ++i) {
             const orc_piece* q = &x.pd[d][i];
             if (q->tensor != ti || !in_box(q, r, c)) continue;
             need[d] += BYTES_PER_ELEM;
             for (int s = 0; s < S; ++s) {
+              if (x.failed[s]) continue;
               int held = 0;
               for (int j = 0; j < x.ns[s]; ++j)
                 if (x.ps[s][j].tensor == ti && in_box(&x.ps[s][j], r, c)) held = 1;
               if (held) {
                 O[(size_t)s * D + d] += BYTES_PER_ELEM;
-                if (sharded) OS[(size_t)s * D + d] += BYTES_PER_ELEM;
+                if (sharded && replica_of(src, s) == replica_of(dst, d) % src->dp)
+                  OS[(size_t)s * D + d] += BYTES_PER_ELEM;
               }
             }
             int snd = sender_of_element(&x, d, q->role, ti, r, c);
             if (snd < 0) {
-              rc = ORC_EUNCOVERED;
+              rc = ORC_EUNRECOVERABLE;
               goto out;
             }
             R[(size_t)snd * D + d] += BYTES_PER_ELEM;
@@ -674,12 +743,16 @@ int orc_matrices_bruteforce(const orc_model* m, const orc_cfg* src, const orc_cf
       }
     }
   }
-  if (route) memcpy(route, R, (size_t)S * D * 8);
+  if (route_m) memcpy(route_m, R, (size_t)S * D * 8);
   if (overlap) memcpy(overlap, O, (size_t)S * D * 8);
   if (overlap_sh) memcpy(overlap_sh, OS, (size_t)S * D * 8);
   if (cost)
     for (int d = 0; d < D; ++d)
-      for (int s = 0; s < S; ++s) cost[(size_t)d * S + s] = need[d] - O[(size_t)s * D + d];
+      for (int s = 0; s < S; ++s)
+        cost[(size_t)d * S + s] =
+            (x.failed[s] || replica_of(src, s) != replica_of(dst, d))
+                ? ORC_COST_INF
+                : need[d] - O[(size_t)s * D + d];
 out:
   free(R); free(O); free(OS); free(need);
   ctx_free(&x);
@@ -708,7 +781,9 @@ static int message_boxes(const ctx_t* x, int s, int d, orc_mbox* out, uint64_t* 
       int pp, tp;
       coords(&x->dst, d, &pp, &tp);
       if (!holds_item(x, &x->dst, pp, tp, t, q->role, a)) continue;
-      if (sender_of_item(x, d, q->role, t, a) != s) continue;
+      const int snd = sender_of_item(x, d, q->role, t, a);
+      if (snd < 0) return ORC_EUNRECOVERABLE;
+      if (snd != s) continue;
       if (first < 0) first = a;
       else if (a != last + 1) return ORC_EBOX;
       last = a;
@@ -744,10 +819,10 @@ static int message_boxes(const ctx_t* x, int s, int d, orc_mbox* out, uint64_t* 
  * (unpadded, = ROUTE[s][d]), the padded message bytes, and the byte
  * displacement of the message (messages in destination order, each at a
  * multiple of 256 bytes).  *total = buffer length. */
-int orc_send_layout(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+int orc_send_layout(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const orc_route* route,
                     int s, uint64_t* count, uint64_t* padded, uint64_t* displ, uint64_t* total) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   if (s < 0 || s >= x.S) {
     ctx_free(&x);
@@ -773,10 +848,10 @@ int orc_send_layout(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, 
 }
 
 /* Message s->d as a list of boxes (for tests and sampled checks). */
-int orc_message(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+int orc_message(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const orc_route* route,
                 int s, int d, orc_mbox* out, int cap, uint64_t* npad) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   if (s < 0 || s >= x.S || d < 0 || d >= x.D) {
     ctx_free(&x);
@@ -803,11 +878,11 @@ int orc_message(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, cons
  * Full tensors are materialized from all resident sources (replicas compared
  * bit for bit), then cut.  A needed element that no resident source covers
  * is an error. */
-int orc_migrate(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+int orc_migrate(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const orc_route* route,
                 const void* const* src_arenas, void* const* dst_arenas,
                 void* const* send_bufs, int t_lo, int t_hi) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   if (t_lo < 0) t_lo = 0;
   if (t_hi > x.nt || t_hi < 0) t_hi = x.nt;
@@ -863,7 +938,7 @@ int orc_migrate(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, cons
     }
     /* 1. materialize from every resident source shard */
     for (int s = 0; s < S; ++s) {
-      if (!src_arenas || !src_arenas[(size_t)s * 4]) continue;
+      if (!src_arenas || !src_arenas[(size_t)s * 4] || x.failed[s]) continue;
       for (int i = 0; i < x.ns[s]; ++i) {
         const orc_piece* p = &x.ps[s][i];
         if (p->tensor != ti) continue;
@@ -976,10 +1051,10 @@ static int find_src_piece(const ctx_t* x, int s, int t, int64_t r, int64_t c) {
 /* For destination d and arena element offsets offs[0..n): the source rank
  * whose element ends up there (by the sender rule) and that element's offset
  * in the source arena.  Gap offsets get src_rank -1. */
-int orc_dst_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+int orc_dst_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const orc_route* route,
                    int d, const uint64_t* offs, int64_t n, int32_t* src_rank, uint64_t* src_off) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   if (d < 0 || d >= x.D) {
     ctx_free(&x);
@@ -1015,10 +1090,10 @@ int orc_dst_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, c
 /* For message s->d and element positions pos[0..n) inside a kind section:
  * the offset in source s's arena of the element stored there, or
  * UINT64_MAX for zero padding / past the end. */
-int orc_msg_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const int32_t* pair,
+int orc_msg_origin(const orc_model* m, const orc_cfg* src, const orc_cfg* dst, const orc_route* route,
                    int s, int d, const uint64_t* pos, int64_t n, uint64_t* src_off) {
   ctx_t x;
-  int rc = ctx_init(&x, m, src, dst, pair);
+  int rc = ctx_init(&x, m, src, dst, route);
   if (rc) return rc;
   if (s < 0 || s >= x.S || d < 0 || d >= x.D) {
     ctx_free(&x);

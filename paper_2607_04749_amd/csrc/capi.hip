@@ -35,10 +35,12 @@ void release_device(etc_plan_t* P) {
   if (P->d_boxes) (void)hipFree(P->d_boxes);
   if (P->d_route_tensors) (void)hipFree(P->d_route_tensors);
   if (P->d_home) (void)hipFree(P->d_home);
+  if (P->d_failed) (void)hipFree(P->d_failed);
   if (have_prev && prev != P->device) (void)hipSetDevice(prev);
   P->d_boxes = nullptr;
   P->d_route_tensors = nullptr;
   P->d_home = nullptr;
+  P->d_failed = nullptr;
 }
 
 int check_device_plan(const etc_plan_t* P) {
@@ -138,6 +140,13 @@ int upload(etc_plan_t* P, int rank) {
   if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
   e = hipMemcpy(P->d_home, P->home.data(), P->home.size() * sizeof(int32_t), hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy (pairing)");
+  if (!P->failed_bits.empty()) {
+    e = hipMalloc(&P->d_failed, P->failed_bits.size() * sizeof(uint32_t));
+    if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    e = hipMemcpy(P->d_failed, P->failed_bits.data(), P->failed_bits.size() * sizeof(uint32_t),
+                  hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy (failed ranks)");
+  }
   return ETC_OK;
 }
 
@@ -178,28 +187,47 @@ int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* tota
 }
 
 int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
-             const int32_t* pair, int rank, uint32_t flags, etc_plan_t** out) {
+             const etc_plan_options* opt, etc_plan_t** out) {
   if (!out) return fail(ETC_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (!model || !src || !dst) return fail(ETC_ERR_INVALID_ARG, "model, src and dst must not be NULL");
+  const etc_plan_options defaults{nullptr, nullptr, 0, ETC_ALL_RANKS, 0};
+  if (!opt) opt = &defaults;
+  const int32_t* pair = opt->pair;
+  const int rank = opt->rank;
+  const uint32_t flags = opt->flags;
   if (flags & ~uint32_t(ETC_PLAN_HOST_ONLY | ETC_PLAN_SKETCH)) return fail(ETC_ERR_INVALID_ARG, "unknown plan flags");
   if (pair && (flags & ETC_PLAN_SKETCH)) return fail(ETC_ERR_INVALID_ARG, "pass a pairing or ETC_PLAN_SKETCH, not both");
+  if (opt->num_failed < 0 || (opt->num_failed > 0 && !opt->failed))
+    return fail(ETC_ERR_INVALID_ARG, "bad failed-rank list");
   std::unique_ptr<etc_plan_t> P;
   try {
     etc::validate(*model, *src, *dst);
     P.reset(new etc_plan_t());
     P->model = *model;
-    P->src = etc::Grid{src->tp, src->pp};
-    P->dst = etc::Grid{dst->tp, dst->pp};
+    P->src = etc::Grid{src->tp, src->pp, src->dp};
+    P->dst = etc::Grid{dst->tp, dst->pp, dst->dp};
     P->rank = rank;
     P->flags = flags;
     const int S = P->src.world(), D = P->dst.world();
+    std::vector<char> dead(S, 0);
+    if (opt->num_failed > 0) {
+      P->failed_bits.assign((S + 31) / 32, 0u);
+      for (int i = 0; i < opt->num_failed; ++i) {
+        const int f = opt->failed[i];
+        if (f < 0 || f >= S) return fail(ETC_ERR_INVALID_ARG, "failed rank " + std::to_string(f) + " out of range");
+        dead[f] = 1;
+        P->failed_bits[f >> 5] |= 1u << (f & 31);
+      }
+    }
     P->tensors = etc::build_tensor_table(P->model);
     etc::build_route_tensors(*P);
     P->home.assign(D, -1);
     if (flags & ETC_PLAN_SKETCH) {
       const std::vector<uint64_t> cost = etc::host_cost_matrix(*P);
       etc::solve_sketch(cost.data(), D, S, P->home.data());
+      for (int d = 0; d < D; ++d)  // a pair across replicas or with a dead rank is no pair
+        if (P->home[d] >= 0 && cost[size_t(d) * S + P->home[d]] >= uint64_t(ETC_COST_INF)) P->home[d] = -1;
     } else if (pair) {
       std::vector<char> taken(S, 0);
       for (int d = 0; d < D; ++d) {
@@ -207,10 +235,14 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
           return fail(ETC_ERR_INVALID_ARG, "pair[" + std::to_string(d) + "] is not a source rank or -1");
         if (pair[d] >= 0 && taken[pair[d]]++)
           return fail(ETC_ERR_INVALID_ARG, "source rank " + std::to_string(pair[d]) + " is paired twice");
+        if (pair[d] >= 0 && (dead[pair[d]] || P->src.replica(pair[d]) != P->dst.replica(d)))
+          return fail(ETC_ERR_INVALID_ARG, "pair[" + std::to_string(d) +
+                                               "] joins a failed rank or another data-parallel replica");
         P->home[d] = pair[d];
       }
-    } else {
-      for (int d = 0; d < D && d < S; ++d) P->home[d] = d;  // identity pairing
+    } else {  // identity pairing, where it stays inside one live replica
+      for (int d = 0; d < D && d < S; ++d)
+        if (!dead[d] && P->src.replica(d) == P->dst.replica(d)) P->home[d] = d;
     }
     if (rank != ETC_ALL_RANKS && (rank < 0 || rank >= num_processes(P.get())))
       return fail(ETC_ERR_RANK, "process " + std::to_string(rank) + " is out of range");
@@ -337,9 +369,10 @@ int etc_cost_matrix(const etc_plan_t* P, int which, uint64_t* d_out, void* strea
   if (which < ETC_CM_ROUTE || which > ETC_CM_COST) return fail(ETC_ERR_INVALID_ARG, "bad matrix selector");
   if (!d_out) return fail(ETC_ERR_INVALID_ARG, "d_out is NULL");
   if (!aligned(d_out, 8)) return fail(ETC_ERR_ALIGN, "d_out is not 8-byte aligned");
-  hipError_t e = etc::launch_cost(P->d_route_tensors, int(P->route_tensors.size()), P->d_home,
-                                  P->src.world(), P->dst.world(), P->src.tp, P->dst.tp, which,
-                                  d_out, static_cast<hipStream_t>(stream));
+  const etc::RouteCtx ctx{P->src.tp, P->src.pp, P->src.dp, P->dst.tp, P->dst.pp, P->dst.dp,
+                         P->d_failed};
+  hipError_t e = etc::launch_cost(P->d_route_tensors, int(P->route_tensors.size()), P->d_home, ctx,
+                                  which, d_out, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "cost matrix launch");
   return ETC_OK;
 }
@@ -350,6 +383,7 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
   if (s < 0 || s >= P->src.world()) return fail(ETC_ERR_RANK, "source rank out of range");
   const etc::CopyTable& t = P->pack_tab[s];
   if (!t.built) return fail(ETC_ERR_RANK, "source rank " + std::to_string(s) + " is not built into this plan");
+  if (t.ntiles == 0) return ETC_OK;  // routes nothing (e.g. a failed rank): nothing is read
   if ((rc = check_arenas(src_arena, "src_arena"))) return rc;
   if (!send_buf) return fail(ETC_ERR_INVALID_ARG, "send_buf is NULL");
   if (!aligned(send_buf, 256)) return fail(ETC_ERR_ALIGN, "send_buf is not 256-byte aligned");

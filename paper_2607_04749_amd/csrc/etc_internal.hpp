@@ -28,9 +28,15 @@ struct LogicalTensor {
   bool fused = false;     // stored right after the previous tensor (up after gate)
 };
 
+// A parallel configuration.  rank = dp * (pp * tp) + pp_i * tp + tp_i: TP
+// fastest, then PP, each data-parallel replica a contiguous block of ranks.
 struct Grid {
-  int tp = 1, pp = 1;
-  int world() const { return tp * pp; }
+  int tp = 1, pp = 1, dp = 1;
+  int world() const { return tp * pp * dp; }
+  int replica_size() const { return tp * pp; }
+  int replica(int rank) const { return rank / (tp * pp); }
+  int pp_of(int rank) const { return (rank % (tp * pp)) / tp; }
+  int tp_of(int rank) const { return rank % tp; }
 };
 
 struct Piece {
@@ -103,8 +109,15 @@ constexpr int kCmThreads = 256;
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
                        uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, bool sectioned,
                        void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
-hipError_t launch_cost(const RouteTensor* rt, int nt, const int32_t* home, int S, int D, int tps,
-                       int tpd, int which, uint64_t* out, hipStream_t stream);
+// Routing context of a plan: both grids and the failed source ranks (bitmap,
+// nullptr when none).  Device copies point at device memory.
+struct RouteCtx {
+  int tps, pps, dps, tpd, ppd, dpd;
+  const uint32_t* failed;
+};
+
+hipError_t launch_cost(const RouteTensor* rt, int nt, const int32_t* home, RouteCtx ctx,
+                       int which, uint64_t* out, hipStream_t stream);
 
 }  // namespace etc
 
@@ -118,6 +131,7 @@ struct etc_plan_s {
   std::vector<etc::RouteTensor> route_tensors;
   std::vector<etc::RankLayout> src_layout, dst_layout;
   std::vector<int32_t> home;  // [d]: source rank paired with target d (migration sketch), or -1
+  std::vector<uint32_t> failed_bits;  // bitmap of source ranks whose states are lost
 
   // messages, indexed [s * D + d]
   struct MsgBox {
@@ -142,6 +156,7 @@ struct etc_plan_s {
   uint32_t copy_lds_reserve = 0;  // dynamic LDS per copy workgroup (occupancy cap)
   etc::RouteTensor* d_route_tensors = nullptr;
   int32_t* d_home = nullptr;  // device copy of home (D entries)
+  uint32_t* d_failed = nullptr;  // device copy of failed_bits
   etc::CopyBox* d_boxes = nullptr;
   std::vector<etc::CopyTable> pack_tab, unpack_tab;
 };

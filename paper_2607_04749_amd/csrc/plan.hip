@@ -105,7 +105,7 @@ int stage_of(const LogicalTensor& t, int role, const Grid& g, int num_layers) {
 RankLayout build_layout(const std::vector<LogicalTensor>& T, const Grid& g, int num_layers,
                         int rank) {
   RankLayout L;
-  const int pp = rank / g.tp, tp = rank % g.tp;
+  const int pp = g.pp_of(rank), tp = g.tp_of(rank);  // every replica has the same layout
   const int nt = int(T.size());
   L.piece_of_tensor[0].assign(nt, -1);
   L.piece_of_tensor[1].assign(nt, -1);
@@ -148,9 +148,10 @@ namespace {
 
 void fail(int code, const std::string& msg) { throw PlanError(code, msg); }
 
-void check_inputs(const etc_model_desc& m, const Grid& g, const char* which, int dp) {
-  if (dp != 1) fail(ETC_ERR_UNSUPPORTED, std::string(which) + ": data parallel size must be 1");
-  if (g.tp < 1 || g.pp < 1) fail(ETC_ERR_INVALID_ARG, std::string(which) + ": tp and pp must be >= 1");
+void check_inputs(const etc_model_desc& m, const Grid& g, const char* which) {
+  if (g.tp < 1 || g.pp < 1 || g.dp < 1)
+    fail(ETC_ERR_INVALID_ARG, std::string(which) + ": tp, pp and dp must be >= 1");
+  if (int64_t(g.tp) * g.pp * g.dp > 65536) fail(ETC_ERR_UNSUPPORTED, std::string(which) + ": more than 65536 ranks");
   auto need = [&](bool ok, const std::string& what) {
     if (!ok)
       fail(ETC_ERR_INDIVISIBLE, std::string(which) + " (tp=" + std::to_string(g.tp) + ", pp=" +
@@ -240,6 +241,7 @@ void build_host_plan(etc_plan_t& P) {
 
   if (P.route_tensors.size() != size_t(nt)) build_route_tensors(P);
 
+  const RouteCtx ctx = host_route_ctx(P);
   // Route every target piece: per target rank, per piece in arena order, the
   // sources that send part of it.  Messages list boxes in that order.
   P.msg.assign(size_t(S) * D, {});
@@ -250,7 +252,7 @@ void build_host_plan(etc_plan_t& P) {
       const RouteTensor& rt = P.route_tensors[q.tensor];
       uint64_t got = 0;
       for (int s = 0; s < S; ++s) {
-        const Span x = routed_span(rt, s, d, P.home[d], P.src.tp, P.dst.tp);
+        const Span x = routed_span(rt, s, d, P.home[d], ctx);
         if (x.len() == 0) continue;
         etc_plan_s::MsgBox b{};
         b.tensor = q.tensor;
@@ -275,7 +277,8 @@ void build_host_plan(etc_plan_t& P) {
         got += n;
       }
       if (got != q.elems())
-        fail(ETC_ERR_INVALID_ARG, "internal: target piece not covered exactly once");
+        fail(ETC_ERR_UNRECOVERABLE, "no live source rank holds part of " + P.tensors[q.tensor].name +
+                                        " needed by target rank " + std::to_string(d));
     }
   }
   P.msg_displ.assign(size_t(S) * D, 0);
@@ -321,7 +324,7 @@ std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<in
     if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "one source feeds more than ETC_MAX_PEERS targets");
     peers->push_back(d);
     for (const auto& b : P.msg[sd]) {
-      const int role_s = role_on(P.route_tensors[b.tensor].src_stage, s / P.src.tp);
+      const int role_s = role_on(P.route_tensors[b.tensor].src_stage, P.src.pp_of(s));
       const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
       const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
       CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
@@ -382,7 +385,7 @@ void build_route_tensors(etc_plan_t& P) {
     r.rows = t.rows;
     r.cols = t.cols;
     r.split = t.split;
-    int copies_src = 0, copies_dst = 0;
+    int copies_src = 0, copies_dst = 0;  // copies within one data-parallel replica
     for (int role = 0; role < 2; ++role) {
       r.src_stage[role] = stage_of(t, role, P.src, P.model.num_layers);
       r.dst_stage[role] = stage_of(t, role, P.dst, P.model.num_layers);
@@ -397,15 +400,26 @@ void build_route_tensors(etc_plan_t& P) {
   }
 }
 
+RouteCtx host_route_ctx(const etc_plan_t& P) {
+  return RouteCtx{P.src.tp, P.src.pp, P.src.dp, P.dst.tp, P.dst.pp, P.dst.dp,
+                  P.failed_bits.empty() ? nullptr : P.failed_bits.data()};
+}
+
 std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P) {
   // COST[d][s] = bytes(d) - OVERLAP[s][d], the same interval arithmetic as
-  // the cost kernel, on the host (feeds the migration sketch at plan time)
+  // the cost kernel, on the host (feeds the migration sketch at plan time);
+  // ETC_COST_INF across data-parallel replicas and to failed ranks
   const int S = P.src.world(), D = P.dst.world();
+  const RouteCtx ctx = host_route_ctx(P);
   std::vector<uint64_t> cost(size_t(D) * S, 0);
   for (int d = 0; d < D; ++d) {
-    const int pp_d = d / P.dst.tp, tp_d = d % P.dst.tp;
+    const int pp_d = P.dst.pp_of(d), tp_d = P.dst.tp_of(d);
     for (int s = 0; s < S; ++s) {
-      const int pp_s = s / P.src.tp, tp_s = s % P.src.tp;
+      if (rank_dead(ctx, s) || P.src.replica(s) != P.dst.replica(d)) {
+        cost[size_t(d) * S + s] = ETC_COST_INF;
+        continue;
+      }
+      const int pp_s = P.src.pp_of(s), tp_s = P.src.tp_of(s);
       uint64_t need = 0, ov = 0;
       for (const RouteTensor& t : P.route_tensors) {
         if (role_on(t.dst_stage, pp_d) < 0) continue;
@@ -424,8 +438,8 @@ std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P) {
 
 void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst) {
   check_model(m);
-  check_inputs(m, Grid{src.tp, src.pp}, "source config", src.dp);
-  check_inputs(m, Grid{dst.tp, dst.pp}, "target config", dst.dp);
+  check_inputs(m, Grid{src.tp, src.pp, src.dp}, "source config");
+  check_inputs(m, Grid{dst.tp, dst.pp, dst.dp}, "target config");
 }
 
 }  // namespace etc

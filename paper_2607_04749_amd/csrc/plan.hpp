@@ -22,6 +22,8 @@ RankLayout build_layout(const std::vector<LogicalTensor>& T, const Grid& g, int 
 void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst);
 // per-tensor routing records (stages per copy role, single-copy flag)
 void build_route_tensors(etc_plan_t& P);
+// routing context of a plan's host tables
+RouteCtx host_route_ctx(const etc_plan_t& P);
 // COST (D x S, bytes) on the host, for the migration sketch
 std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P);
 // layouts, routing, message layouts (host only); P.home must be set

@@ -27,6 +27,8 @@ PLAN_HOST_ONLY = 1
 PLAN_SKETCH = 2
 OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP = \
     0, -1, -2, -3, -4, -5, -6, -7
+ERR_UNRECOVERABLE = -8
+COST_INF = 1 << 50
 MAX_PEERS = 256
 ESIZE = (2, 4, 4, 4)
 
@@ -39,6 +41,11 @@ class ModelDesc(ctypes.Structure):
 
 class ParallelCfg(ctypes.Structure):
     _fields_ = [("tp", ctypes.c_int32), ("pp", ctypes.c_int32), ("dp", ctypes.c_int32)]
+
+
+class PlanOptions(ctypes.Structure):
+    _fields_ = [("pair", ctypes.c_void_p), ("failed", ctypes.c_void_p),
+                ("num_failed", ctypes.c_int32), ("rank", ctypes.c_int32), ("flags", ctypes.c_uint32)]
 
 
 class PieceInfo(ctypes.Structure):
@@ -70,7 +77,7 @@ def _load():
     L = ctypes.CDLL(LIB_PATH)
     vp, i32p, u64p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_uint64)
     L.etc_plan.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(ParallelCfg),
-                           ctypes.POINTER(ParallelCfg), vp, ctypes.c_int, ctypes.c_uint32,
+                           ctypes.POINTER(ParallelCfg), ctypes.POINTER(PlanOptions),
                            ctypes.POINTER(vp)]
     L.etc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
     L.etc_plan_pairing.argtypes = [vp, vp]
@@ -234,18 +241,21 @@ def etc_sketch(cost):
     return pr, tot.value
 
 
-def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None):
+def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None, failed=None):
     """model: object with astuple() (arch, layers, hidden, heads, kv_heads, ffn,
     vocab, max_pos, tied, flags); src/dst: objects with astuple() (tp, pp, dp);
-    pair: None (identity), or D entries (old rank per new rank, -1 = none)."""
+    pair: None (identity), or D entries (old rank per new rank, -1 = none);
+    failed: old ranks whose states are lost."""
     m = ModelDesc(*model.astuple())
     a = ParallelCfg(*src.astuple())
     b = ParallelCfg(*dst.astuple())
     h = ctypes.c_void_p()
     pr = None if pair is None else np.ascontiguousarray(pair, np.int32)
-    _check(_lib.etc_plan(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b),
-                         None if pr is None else pr.ctypes.data, rank, flags, ctypes.byref(h)),
-           "etc_plan")
+    fl = np.ascontiguousarray(failed if failed else [0], np.int32)
+    opt = PlanOptions(None if pr is None else pr.ctypes.data, fl.ctypes.data,
+                      len(failed) if failed else 0, rank, flags)
+    _check(_lib.etc_plan(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), ctypes.byref(opt),
+                         ctypes.byref(h)), "etc_plan")
     return Plan(h, model, src, dst, rank)
 
 

@@ -82,7 +82,7 @@ def test_piece_names_and_shapes():
     (MICRO_MODELS["gpt"], Parallel(3, 1), Parallel(1, 1), etc.ERR_INDIVISIBLE),
     (MICRO_MODELS["gpt"], Parallel(1, 3), Parallel(1, 1), etc.ERR_INDIVISIBLE),
     (MICRO_MODELS["gpt"], Parallel(1, 1), Parallel(8, 1), etc.ERR_INDIVISIBLE),
-    (MICRO_MODELS["gpt"], Parallel(1, 1, 2), Parallel(1, 1), etc.ERR_UNSUPPORTED),
+    (MICRO_MODELS["gpt"], Parallel(1, 1, 0), Parallel(1, 1), etc.ERR_INVALID_ARG),
     (MICRO_MODELS["gpt"], Parallel(0, 1), Parallel(1, 1), etc.ERR_INVALID_ARG),
     (ModelShape(GPT, 4, 16, 4, 2, 32, 16, 8, 1), Parallel(1, 1), Parallel(1, 1), etc.ERR_UNSUPPORTED),
     (ModelShape(LLAMA, 4, 16, 4, 3, 32, 16, 0, 0), Parallel(1, 1), Parallel(1, 1), etc.ERR_INVALID_ARG),

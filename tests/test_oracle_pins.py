@@ -434,8 +434,8 @@ def test_error_codes():
         oracle.matrices(m, Parallel(1, 3), Parallel(1, 1))
     assert e.value.code == oracle.EINDIV
     with pytest.raises(oracle.OracleError) as e:
-        oracle.matrices(m, Parallel(1, 1, 2), Parallel(1, 1))
-    assert e.value.code == oracle.EUNSUP
+        oracle.matrices(m, Parallel(1, 1, 0), Parallel(1, 1))
+    assert e.value.code == oracle.EINVAL
     with pytest.raises(oracle.OracleError) as e:
         oracle.layout(m, Parallel(2, 1), 2)
     assert e.value.code == oracle.ERANK
