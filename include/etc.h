@@ -181,8 +181,10 @@ ETC_API int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64
 typedef struct {
   const int32_t* pair;   /* D entries, host: pair[d] = the old rank whose GPU
                             becomes new rank d, or -1 for a new GPU; each old
-                            rank at most once, never across data-parallel
-                            replicas or with a failed rank.  NULL: identity
+                            rank at most once, never a failed rank.  It may
+                            cross data-parallel replicas (all replicas hold
+                            the same states), as a coalesced pairing does;
+                            the sketch never does.  NULL: identity
                             pairing (d with d, where both lie in the same
                             replica and d is alive), or the optimal sketch
                             with ETC_PLAN_SKETCH */
@@ -212,6 +214,30 @@ typedef struct {
  * needed data failed), RANK, NOMEM, HIP. */
 ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
                      const etc_parallel_cfg* dst, const etc_plan_options* opt, etc_plan_t** out);
+
+/* Virtual rank allocator (Sec. III-E, Algorithm 2): de-fragment the devices
+ * after the plan's migration.  The migration leaves new rank d on the device
+ * of its paired old rank; unpaired new ranks start on fresh devices numbered
+ * S, S+1, ... in order of d (S = old world size).  Devices of failed old
+ * ranks are gone and take part in nothing.  mode:
+ *  ETC_DEFRAG_OCCUPANCY: idle live devices, in ascending order, take over the
+ *    processes of occupied devices, in descending order, while the idle device
+ *    precedes the occupied one, so the occupied devices end up first and whole
+ *    nodes at the end are freed (whatever the node size);
+ *  ETC_DEFRAG_EFFICIENCY: the k-th live device (old ones ascending, then fresh
+ *    ones) hosts new rank k, so a TP group (consecutive ranks) shares a node
+ *    whenever TP divides the node size;
+ *  ETC_DEFRAG_NONE: no remapping.
+ * Out (host arrays): placement[d] (D entries) = final device of new rank d;
+ * ops (optional, 3 * D entries) = remap operators (rank, from device, to
+ * device), *nops of them; coalesced (optional, D entries) = the coalesced
+ * pairing (Sec. III-E): placement[d] where that is an old device (< S), else
+ * -1.  A plan built with it migrates straight to the final devices, in place
+ * of the migration followed by the remap, and yields the same target states.
+ * Host only.  Errors: INVALID_ARG. */
+enum { ETC_DEFRAG_NONE = 0, ETC_DEFRAG_OCCUPANCY = 1, ETC_DEFRAG_EFFICIENCY = 2 };
+ETC_API int etc_plan_defrag(const etc_plan_t* plan, int mode, int32_t* placement, int32_t* ops,
+                            int* nops, int32_t* coalesced);
 
 /* The plan's pairing: pair[d] (D entries) = old rank paired with new rank d, or -1. */
 ETC_API int etc_plan_pairing(const etc_plan_t* plan, int32_t* pair);

@@ -98,6 +98,8 @@ def lib():
         L.orc_dst_origin.argtypes = [mp, cp, cp, vp, ctypes.c_int, vp, ctypes.c_int64, vp, vp]
         L.orc_msg_origin.argtypes = [mp, cp, cp, vp, ctypes.c_int, ctypes.c_int, vp, ctypes.c_int64, vp]
         L.orc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
+        L.orc_defrag.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp, ctypes.c_int, ctypes.c_int,
+                                 ctypes.c_int, vp, vp, ctypes.POINTER(ctypes.c_int)]
         _lib = L
     return _lib
 
@@ -257,3 +259,20 @@ def sketch(cost):
     tot = ctypes.c_uint64()
     _check(lib().orc_sketch(_ptr(c), M, N, _ptr(pair), ctypes.byref(tot)), "sketch")
     return pair, tot.value
+
+
+DEFRAG_NONE, DEFRAG_OCCUPANCY, DEFRAG_EFFICIENCY = 0, 1, 2
+
+
+def defrag(S, D, pair, failed=None, n=8, mode=DEFRAG_OCCUPANCY):
+    """Placement-aware remapping (Algorithm 2) after a migration with the given
+    pairing: (placement int32[D] = final device of each new rank, operators as
+    a list of (rank, from device, to device))."""
+    pa = np.ascontiguousarray(pair, np.int32)
+    fa = np.ascontiguousarray(failed if failed else [0], np.int32)
+    placement = np.zeros(D, np.int32)
+    ops = np.zeros(3 * D, np.int32)
+    nops = ctypes.c_int()
+    _check(lib().orc_defrag(S, D, _ptr(pa), _ptr(fa), len(failed) if failed else 0, n, mode,
+                            _ptr(placement), _ptr(ops), ctypes.byref(nops)), "defrag")
+    return placement, [tuple(int(v) for v in ops[3 * i:3 * i + 3]) for i in range(nops.value)]

@@ -23,6 +23,8 @@
  *    from the source that the sender rule names.
  *  - States by workload type (Sec. III-D): bf16 parameter, fp32 master,
  *    fp32 Adam m, fp32 Adam v, packed when sent and unpacked after.
+ *  - Placement-aware remapping of the virtual rank allocator (Sec. III-E,
+ *    Algorithm 2).
  *  - The migration result itself: the plain definition.  Materialize each
  *    full logical tensor from the resident source shards (replicas must agree
  *    bit for bit), then cut every destination piece and every message box out
@@ -339,8 +341,10 @@ static void ctx_free(ctx_t* x) {
 
 /* route: pairing and failed ranks (NULL = identity pairing, no failures).
  * Under the identity pairing target d pairs with source d when both exist
- * and source d is alive.  A pairing may only join ranks of the same data-
- * parallel replica, and never a failed rank. */
+ * and source d is alive and in the same data-parallel replica.  A given
+ * pairing never names a failed rank; it may join ranks of different replicas
+ * (every replica holds the same states), which a coalesced pairing does
+ * (Sec. III-E). */
 static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_cfg* dst,
                     const orc_route* route) {
   const int32_t* pair = route ? route->pair : NULL;
@@ -391,8 +395,7 @@ static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_
       ctx_free(x);
       return ORC_EINVAL;
     }
-    if (x->home[d] >= 0 &&
-        (x->failed[x->home[d]] || replica_of(src, x->home[d]) != replica_of(dst, d))) {
+    if (x->home[d] >= 0 && x->failed[x->home[d]]) {
       ctx_free(x);
       return ORC_EINVAL;
     }
@@ -1217,4 +1220,107 @@ int orc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* tota
   if (total) *total = tot;
   free(from); free(to); free(cap); free(w); free(dist); free(via);
   return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* virtual rank allocator (Sec. III-E, Algorithm 2)                          */
+/* ------------------------------------------------------------------------ */
+
+/* Placement-aware remapping after a migration with pairing pair[d] (the old
+ * rank whose device becomes new rank d, or -1).  Devices are grouped n to a
+ * node.  The devices in play, in this order: the live old devices (ids
+ * 0..S-1 without the failed ranks), then one fresh device per new rank that
+ * the pairing leaves unpaired (ids S, S+1, ... in rank order).  p2c[i] is the
+ * new rank hosted by the i-th device after the migration, or -1 (idle).
+ *  mode 1, occupancy: walk the idle devices in order and the occupied devices
+ *    in reverse order, node by node, and pair them until the two walks meet;
+ *    each pair hands the occupied device's process to the idle device.
+ *  mode 2, efficiency: the target placement puts ranks 0..D-1 node by node on
+ *    the devices; a node whose target differs from its loads is fragmented,
+ *    and at every position of it where they differ the target rank is moved
+ *    onto that device.
+ *  mode 0: no remapping.
+ * Out: placement[d] (D) = device finally hosting new rank d; ops (3 entries
+ * per operator: rank, from device, to device; may be NULL), *nops.  The node
+ * size groups the devices only; the result does not depend on it. */
+int orc_defrag(int S, int D, const int32_t* pair, const int32_t* failed, int num_failed, int n,
+               int mode, int32_t* placement, int32_t* ops, int* nops) {
+  if (S < 1 || D < 1 || n < 1 || !pair || !placement || !nops || num_failed < 0) return ORC_EINVAL;
+  if (mode < 0 || mode > 2) return ORC_EINVAL;
+  char* dead = calloc((size_t)S, 1);
+  int32_t* dev = malloc(sizeof(int32_t) * (size_t)(S + D));
+  int32_t* p2c = malloc(sizeof(int32_t) * (size_t)(S + D));
+  int32_t* loc = malloc(sizeof(int32_t) * (size_t)D);
+  int rc = ORC_OK;
+  if (!dead || !dev || !p2c || !loc) { rc = ORC_ENOMEM; goto out; }
+  for (int i = 0; i < num_failed; ++i) {
+    if (failed[i] < 0 || failed[i] >= S) { rc = ORC_EINVAL; goto out; }
+    dead[failed[i]] = 1;
+  }
+  for (int d = 0; d < D; ++d) {
+    if (pair[d] < -1 || pair[d] >= S || (pair[d] >= 0 && dead[pair[d]])) { rc = ORC_EINVAL; goto out; }
+    for (int e = 0; e < d; ++e)
+      if (pair[d] >= 0 && pair[e] == pair[d]) { rc = ORC_EINVAL; goto out; }
+  }
+  /* the device list and what each device hosts after the migration */
+  int nd = 0;
+  for (int v = 0; v < S; ++v) {
+    if (dead[v]) continue;
+    dev[nd] = v;
+    p2c[nd] = -1;
+    for (int d = 0; d < D; ++d)
+      if (pair[d] == v) p2c[nd] = d;
+    ++nd;
+  }
+  int fresh = S;
+  for (int d = 0; d < D; ++d)
+    if (pair[d] < 0) {
+      dev[nd] = fresh++;
+      p2c[nd] = d;
+      ++nd;
+    }
+  for (int i = 0; i < nd; ++i)
+    if (p2c[i] >= 0) loc[p2c[i]] = dev[i];
+  for (int d = 0; d < D; ++d) placement[d] = loc[d];
+  int k = 0;
+#define EMIT(rank, from, to)                   \
+  do {                                         \
+    if (ops) {                                 \
+      ops[3 * k] = (rank);                     \
+      ops[3 * k + 1] = (from);                 \
+      ops[3 * k + 2] = (to);                   \
+    }                                          \
+    placement[(rank)] = (to);                  \
+    ++k;                                       \
+  } while (0)
+  if (mode == 1) {
+    int i = 0, j = nd - 1;
+    for (;;) {
+      while (i < nd && p2c[i] >= 0) ++i;  /* next idle device, in order */
+      while (j >= 0 && p2c[j] < 0) --j;   /* next occupied device, in reverse */
+      if (i >= nd || j < 0 || i > j) break; /* the walks have met */
+      EMIT(p2c[j], dev[j], dev[i]);
+      ++i;
+      --j;
+    }
+  } else if (mode == 2) {
+    const int nodes = (nd + n - 1) / n;
+    for (int node = 0; node < nodes; ++node) {
+      int fragmented = 0;
+      for (int i = node * n; i < node * n + n && i < nd; ++i) {
+        const int target = i < D ? i : -1;
+        if (target != p2c[i]) fragmented = 1;
+      }
+      if (!fragmented) continue;
+      for (int i = node * n; i < node * n + n && i < nd; ++i) {
+        const int target = i < D ? i : -1;
+        if (target >= 0 && target != p2c[i]) EMIT(target, loc[target], dev[i]);
+      }
+    }
+  }
+#undef EMIT
+  *nops = k;
+out:
+  free(dead); free(dev); free(p2c); free(loc);
+  return rc;
 }

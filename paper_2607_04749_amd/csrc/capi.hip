@@ -235,9 +235,8 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
           return fail(ETC_ERR_INVALID_ARG, "pair[" + std::to_string(d) + "] is not a source rank or -1");
         if (pair[d] >= 0 && taken[pair[d]]++)
           return fail(ETC_ERR_INVALID_ARG, "source rank " + std::to_string(pair[d]) + " is paired twice");
-        if (pair[d] >= 0 && (dead[pair[d]] || P->src.replica(pair[d]) != P->dst.replica(d)))
-          return fail(ETC_ERR_INVALID_ARG, "pair[" + std::to_string(d) +
-                                               "] joins a failed rank or another data-parallel replica");
+        if (pair[d] >= 0 && dead[pair[d]])
+          return fail(ETC_ERR_INVALID_ARG, "pair[" + std::to_string(d) + "] is a failed rank");
         P->home[d] = pair[d];
       }
     } else {  // identity pairing, where it stays inside one live replica
@@ -265,6 +264,23 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
   }
   *out = P.release();
   g_last_error.clear();
+  return ETC_OK;
+}
+
+int etc_plan_defrag(const etc_plan_t* P, int mode, int32_t* placement, int32_t* ops, int* nops,
+                    int32_t* coalesced) {
+  if (!P || !placement || !nops) return fail(ETC_ERR_INVALID_ARG, "NULL argument");
+  try {
+    const int S = P->src.world(), D = P->dst.world();
+    std::vector<char> dead(S, 0);
+    for (int s = 0; s < S; ++s)
+      dead[s] = !P->failed_bits.empty() && ((P->failed_bits[s >> 5] >> (s & 31)) & 1u);
+    const int rc = etc::defrag(S, D, P->home.data(), dead, mode, placement, ops, nops);
+    if (rc) return fail(rc, "unknown de-fragmentation mode " + std::to_string(mode));
+    for (int d = 0; coalesced && d < D; ++d) coalesced[d] = placement[d] < S ? placement[d] : -1;
+  } catch (const std::bad_alloc&) {
+    return fail(ETC_ERR_NOMEM, "host allocation failed");
+  }
   return ETC_OK;
 }
 

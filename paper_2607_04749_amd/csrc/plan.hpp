@@ -28,6 +28,9 @@ RouteCtx host_route_ctx(const etc_plan_t& P);
 std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P);
 // layouts, routing, message layouts (host only); P.home must be set
 void build_host_plan(etc_plan_t& P);
+// virtual rank allocator (defrag.hip); returns an ETC_ status
+int defrag(int S, int D, const int32_t* home, const std::vector<char>& dead, int mode,
+           int32_t* placement, int32_t* ops, int* nops);
 // migration sketch (sketch.hip): pair[i] = column paired with row i, or -1
 uint64_t solve_sketch(const uint64_t* cost, int M, int N, int32_t* pair);
 // copy descriptors of one rank (terminated by a sentinel box holding the tile count)

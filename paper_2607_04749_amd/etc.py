@@ -30,6 +30,7 @@ OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_
 ERR_UNRECOVERABLE = -8
 COST_INF = 1 << 50
 MAX_PEERS = 256
+DEFRAG_NONE, DEFRAG_OCCUPANCY, DEFRAG_EFFICIENCY = 0, 1, 2
 ESIZE = (2, 4, 4, 4)
 
 
@@ -81,6 +82,7 @@ def _load():
                            ctypes.POINTER(vp)]
     L.etc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
     L.etc_plan_pairing.argtypes = [vp, vp]
+    L.etc_plan_defrag.argtypes = [vp, ctypes.c_int, vp, vp, i32p, vp]
     L.etc_plan_process.argtypes = [vp, ctypes.c_int, i32p, i32p]
     L.etc_plan_free.argtypes = [vp]
     L.etc_plan_free.restype = None
@@ -208,6 +210,18 @@ class Plan:
         pr = np.zeros(self.D, np.int32)
         _check(_lib.etc_plan_pairing(self.handle, pr.ctypes.data), "etc_plan_pairing")
         return pr
+
+    def defrag(self, mode):
+        """Virtual rank allocator: (placement[d] = final device of new rank d,
+        remap operators as (rank, from device, to device) tuples, the
+        coalesced pairing)."""
+        pl = np.zeros(self.D, np.int32)
+        ops = np.zeros(3 * self.D, np.int32)
+        co = np.zeros(self.D, np.int32)
+        n = ctypes.c_int()
+        _check(_lib.etc_plan_defrag(self.handle, mode, pl.ctypes.data, ops.ctypes.data,
+                                    ctypes.byref(n), co.ctypes.data), "etc_plan_defrag")
+        return pl, [tuple(int(v) for v in ops[3 * i:3 * i + 3]) for i in range(n.value)], co
 
     def process(self, p):
         """(old rank, new rank) of process p, each -1 if none."""

@@ -163,9 +163,6 @@ def test_dp_overlap_sharded_sums():
 def test_dp_errors():
     m = MICRO_MODELS["gpt"]
     w = Parallel(2, 1, 2)
-    with pytest.raises(etc.EtcError) as e:  # pairing across replicas
-        etc.etc_plan(m, w, w, flags=HOST, pair=[2, 3, 0, 1])
-    assert e.value.code == etc.ERR_INVALID_ARG
     with pytest.raises(etc.EtcError) as e:  # pairing with a failed rank
         etc.etc_plan(m, w, w, flags=HOST, pair=[0, 1, 2, 3], failed=[1])
     assert e.value.code == etc.ERR_INVALID_ARG
