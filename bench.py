@@ -40,7 +40,7 @@ def log(*a):
 
 def kernel_hash():
     h = hashlib.sha256()
-    for f in ("copy.hip", "copy_geom.hpp", "etc_internal.hpp", "plan.hip"):
+    for f in ("copy.hip", "copy_geom.hpp", "etc_internal.hpp", "plan.hip", "route.hpp"):
         with open(os.path.join(ROOT, "paper_2607_04749_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -252,6 +252,7 @@ def main():
         "pack_GBps": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1),
         "unpack_GBps": round(unpack_bytes / (unpack_ms * 1e-3) / 1e9, 1),
         "pack_ms": round(pack_ms, 4), "unpack_ms": round(unpack_ms, 4),
+        "pack_bytes": pack_bytes, "unpack_bytes": unpack_bytes,
         "cost_matrix_us": round(cm_us, 2), "cost_matrix_cells": S * D,
         "sketch_us": round(sketch_us, 1), "pairing": "identity" if args.identity else "sketch",
         "d2d_copy_GBps": round(d2d_gbps, 1), "plan_ms": round(plan_ms, 2),
