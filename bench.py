@@ -8,7 +8,15 @@ with old ranks by the optimal migration sketch (ETC_PLAN_SKETCH; --identity
 pairs rank d with rank d); the share is process 0's: the old rank it packs
 and the new rank it becomes.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--identity]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+                    [--identity] [--mode direct|chunked|coalesced]
+
+Modes: direct (default) packs and unpacks all four state kinds in one launch
+each; chunked moves one state kind at a time through per-kind chunk buffers
+(state chunking, Sec. III-D), four pack and four unpack launches per step;
+coalesced plans the migration with the coalesced pairing of occupancy
+de-fragmentation (Sec. III-E) and times the share of the first process that
+takes over a moved rank, which receives that rank's whole state.
 
 Prints one JSON line: value = algorithmic bytes of pack + unpack (each reads
 and writes its routed bytes) per step time, in GB/s; the roofline object is for
@@ -60,24 +68,51 @@ def measured_traffic(workload, kernel, algorithmic):
     return ent.get("bytes_per_launch")
 
 
-def cpu_baseline(w, identity):
-    """The oracle (as it stands, one thread) on the tensors of layer 0 of the
-    same share: materialize + cut for the unpack target and the pack source's
-    messages, routed with the oracle's own migration sketch (or the identity
-    pairing).  Reported in GB/s over the sample's algorithmic bytes."""
+def oracle_pairing(w, pairing):
+    """The pairing as the oracle computes it (None = identity), and, for the
+    coalesced pairing, the (process, new rank) of the first moved rank."""
+    import numpy as np
+
+    import oracle
+
+    m, a, b = w.model, w.src, w.dst
+    if pairing == "identity":
+        return None, None
+    C = oracle.matrices(m, a, b)["cost"]
+    sk = oracle.sketch(C)[0]
+    sk = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)],
+                  np.int32)
+    if pairing == "sketch":
+        return sk, None
+    placement, ops = oracle.defrag(a.world, b.world, sk, mode=oracle.DEFRAG_OCCUPANCY)
+    co = np.where(placement < a.world, placement, -1).astype(np.int32)
+    mv = next(((t, r) for r, _, t in ops if t < a.world), None)
+    return co, mv
+
+
+def cpu_baseline(w, pairing):
+    """The oracle (as it stands, one thread) on the tensors of one layer of the
+    same share (the first layer the target holds): materialize + cut for the
+    unpack target and the pack source's messages, routed with the pairing the
+    oracle computes itself.  Reported in GB/s over the sample's algorithmic
+    bytes."""
     import numpy as np
 
     import oracle
     import synth
 
     m, a, b = w.model, w.src, w.dst
-    pair = None if identity else oracle.sketch(oracle.matrices(m, a, b)["cost"])[0]
-    T = oracle.tensors(m)
-    sample = [i for i, t in enumerate(T) if t["layer"] == 0]
-    t_lo, t_hi = sample[0], sample[-1] + 1
+    pair, mv = oracle_pairing(w, pairing)
     s0 = w.pack_rank
     d0 = w.unpack_rank if pair is None else next((d for d in range(b.world) if pair[d] == s0),
                                                   w.unpack_rank)
+    if mv is not None:
+        s0, d0 = mv
+    T = oracle.tensors(m)
+    layer = min(T[p["tensor"]]["layer"] for p in oracle.layout(m, b, d0)[0]
+                if T[p["tensor"]]["layer"] >= 0)
+    sample = [i for i, t in enumerate(T) if t["layer"] == layer]
+    t_lo, t_hi = sample[0], sample[-1] + 1
     feeders = sorted({s for s in range(a.world)
                       if any(x["tensor"] in sample
                              for x in oracle.message(m, a, b, s, d0, pair=pair)[0])} | {s0})
@@ -98,8 +133,9 @@ def cpu_baseline(w, identity):
     oracle.migrate(m, a, b, src, dst, send, t_lo, t_hi, pair=pair)
     dt = time.perf_counter() - t0
     return {"value": round(alg / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"tensors of layer 0 ({len(sample)} tensors): pack of source {s0} + unpack of "
-                      f"target {d0}, {alg / 1e9:.3f} GB algorithmic, {dt:.2f} s"}
+            "sample": f"tensors of layer {layer} ({len(sample)} tensors): pack of source {s0} + "
+                      f"unpack of target {d0}, {pairing} pairing, {alg / 1e9:.3f} GB algorithmic, "
+                      f"{dt:.2f} s"}
 
 
 def main():
@@ -110,10 +146,14 @@ def main():
     ap.add_argument("--workload", default="llama-70b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--identity", action="store_true", help="identity pairing instead of the sketch")
+    ap.add_argument("--mode", choices=("direct", "chunked", "coalesced"), default="direct")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the migration; runs on more than one GPU "
               "are not part of this build (--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+    if args.identity and args.mode == "coalesced":
+        print("--identity and --mode coalesced exclude each other", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -127,14 +167,28 @@ def main():
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    s0, d0 = w.pack_rank, w.unpack_rank
+    pairing = "identity" if args.identity else ("coalesced" if args.mode == "coalesced" else "sketch")
 
     t0 = time.perf_counter()
-    plan = etc.etc_plan(w.model, w.src, w.dst, flags=0 if args.identity else etc.PLAN_SKETCH)
+    moved = None
+    if args.mode == "coalesced":
+        base = etc.etc_plan(w.model, w.src, w.dst, flags=etc.PLAN_HOST_ONLY | etc.PLAN_SKETCH)
+        _, ops, co = base.defrag(etc.DEFRAG_OCCUPANCY)
+        base.free()
+        moved = next(((t, r) for r, _, t in ops if t < w.src.world), None)
+        if moved is None:
+            print(f"{w.name}: occupancy de-fragmentation moves no rank onto an old device",
+                  file=sys.stderr)
+            sys.exit(2)
+        plan = etc.etc_plan(w.model, w.src, w.dst, pair=co)
+    else:
+        plan = etc.etc_plan(w.model, w.src, w.dst, flags=0 if args.identity else etc.PLAN_SKETCH)
     plan_ms = (time.perf_counter() - t0) * 1e3
     S, D = plan.S, plan.D
     if w.mode == "full":  # every source packs, every target unpacks
         packers, unpackers = list(range(S)), list(range(D))
+    elif moved is not None:  # the process that takes over a moved rank
+        packers, unpackers = [moved[0]], [moved[1]]
     else:  # process 0's share: the old rank it packs, the new rank it becomes
         s0, d0 = plan.process(w.pack_rank)
         if d0 < 0:
@@ -142,53 +196,84 @@ def main():
         packers, unpackers = [s0], [d0]
     feeders = sorted({int(s) for d in unpackers for s in np.nonzero(plan.recv_counts(d))[0]})
     resident = sorted(set(feeders) | set(packers))
-    log(f"{w.name}: {w.src} -> {w.dst}; plan {plan_ms:.1f} ms; resident sources {resident}")
+    log(f"{w.name}: {w.src} -> {w.dst}; mode {args.mode}; plan {plan_ms:.1f} ms; "
+        f"pack {packers if len(packers) < 9 else len(packers)}; "
+        f"unpack {unpackers if len(unpackers) < 9 else len(unpackers)}; resident sources {resident}")
 
     # inputs: seeded states at the layout the library reports for each source
-    src, send = {}, {}
+    src = {}
     for s in resident:
         elems = plan.arena_elems(etc.SIDE_SRC, s)
         src[s] = [torch.zeros(elems * e, dtype=torch.uint8, device=dev) for e in ESIZE]
         pieces = plan.pieces(etc.SIDE_SRC, s)
         fc = {p["tensor"]: p["full_cols"] for p in pieces}
         synth.fill_device(pieces, fc, [x.data_ptr() for x in src[s]], w.seed, stream.cuda_stream)
-        send[s] = torch.zeros(plan.send_layout(s)[3], dtype=torch.uint8, device=dev)
     dst = {d: [torch.zeros(plan.arena_elems(etc.SIDE_DST, d) * e, dtype=torch.uint8, device=dev)
                for e in ESIZE] for d in unpackers}
-    for s in resident:
-        if s not in packers:
-            etc.etc_pack(plan, s, src[s], send[s])
-    layouts = {s: plan.send_layout(s) for s in resident}
-    msgs = {d: [send[s].data_ptr() + int(layouts[s][2][d]) if s in layouts and layouts[s][0][d] else None
-                for s in range(S)] for d in unpackers}
     route = torch.zeros(S * D, dtype=torch.int64, device=dev)
     cost = torch.zeros(S * D, dtype=torch.int64, device=dev)
+
+    # launches of one step: (side, kind or None, rank, callable, algorithmic bytes)
+    launches = []
+    if args.mode == "chunked":
+        lay = {(s, k): plan.chunk_layout(s, k) for s in resident for k in range(4)}
+        buf = {(s, k): torch.zeros(max(lay[s, k][2], 256), dtype=torch.uint8, device=dev)
+               for s in resident for k in range(4)}
+        for s in resident:
+            if s not in packers:
+                for k in range(4):
+                    etc.etc_pack_kind(plan, s, k, src[s][k], buf[s, k])
+        for k in range(4):
+            for s in packers:
+                launches.append(("pack", k, s, lambda s=s, k=k: etc.etc_pack_kind(
+                    plan, s, k, src[s][k], buf[s, k]), 2 * int(lay[s, k][0].sum())))
+            for d in unpackers:
+                msgs = [buf[s, k].data_ptr() + int(lay[s, k][1][d])
+                        if (s, k) in lay and lay[s, k][0][d] else None for s in range(S)]
+                nb = 2 * sum(int(lay[s, k][0][d]) for s in resident if (s, k) in lay)
+                launches.append(("unpack", k, d, lambda d=d, k=k, msgs=msgs: etc.etc_unpack_kind(
+                    plan, d, k, msgs, dst[d][k]), nb))
+        stage_bytes = sum(int(x.numel()) for x in buf.values())
+    else:
+        send = {s: torch.zeros(plan.send_layout(s)[3], dtype=torch.uint8, device=dev)
+                for s in resident}
+        for s in resident:
+            if s not in packers:
+                etc.etc_pack(plan, s, src[s], send[s])
+        layouts = {s: plan.send_layout(s) for s in resident}
+        for s in packers:
+            launches.append(("pack", None, s, lambda s=s: etc.etc_pack(plan, s, src[s], send[s]),
+                             2 * int(layouts[s][0].sum())))
+        for d in unpackers:
+            msgs = [send[s].data_ptr() + int(layouts[s][2][d]) if s in layouts and layouts[s][0][d]
+                    else None for s in range(S)]
+            launches.append(("unpack", None, d, lambda d=d, msgs=msgs: etc.etc_unpack(
+                plan, d, msgs, dst[d]), 2 * int(plan.recv_counts(d).sum())))
+        stage_bytes = sum(int(x.numel()) for x in send.values())
     torch.cuda.synchronize()
     log(f"inputs resident: {sum(x.numel() for v in src.values() for x in v) / 1e9:.1f} GB sources, "
-        f"{sum(x.numel() for v in dst.values() for x in v) / 1e9:.1f} GB targets")
+        f"{sum(x.numel() for v in dst.values() for x in v) / 1e9:.1f} GB targets, "
+        f"{stage_bytes / 1e9:.1f} GB message buffers")
 
-    pack_bytes = 2 * sum(int(layouts[s][0].sum()) for s in packers)
-    unpack_bytes = 2 * sum(int(plan.recv_counts(d).sum()) for d in unpackers)
+    pack_bytes = sum(l[4] for l in launches if l[0] == "pack")
+    unpack_bytes = sum(l[4] for l in launches if l[0] == "unpack")
     alg_bytes = pack_bytes + unpack_bytes
 
     def step(ev=None):
         etc.etc_cost_matrix(plan, etc.CM_ROUTE, route)
         etc.etc_cost_matrix(plan, etc.CM_COST, cost)
+        for i, l in enumerate(launches):
+            if ev:
+                ev[i].record(stream)
+            l[3]()
         if ev:
-            ev[0].record(stream)
-        for s in packers:
-            etc.etc_pack(plan, s, src[s], send[s])
-        if ev:
-            ev[1].record(stream)
-        for d in unpackers:
-            etc.etc_unpack(plan, d, msgs[d], dst[d])
-        if ev:
-            ev[2].record(stream)
+            ev[-1].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)]
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -196,8 +281,10 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    pack_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    unpack_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    launch_ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+                 for i in range(len(launches))]
+    pack_ms = sum(t for t, l in zip(launch_ms, launches) if l[0] == "pack")
+    unpack_ms = sum(t for t, l in zip(launch_ms, launches) if l[0] == "unpack")
 
     # cost matrices alone (events around a burst of launches)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -217,7 +304,7 @@ def main():
         ts.append(time.perf_counter() - t1)
     sketch_us = sorted(ts)[2] * 1e6
 
-    # practical ceiling: a plain device-to-device copy of the unpack's bytes
+    # practical ceiling: a plain device-to-device copy of half the unpack's bytes
     nb = unpack_bytes // 2
     a_buf = torch.empty(nb, dtype=torch.uint8, device=dev)
     b_buf = torch.empty(nb, dtype=torch.uint8, device=dev)
@@ -230,40 +317,50 @@ def main():
     d2d_gbps = 2 * nb * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del a_buf, b_buf
 
-    # dominant copy launch: per-launch average of the side taking longer
-    if unpack_ms >= pack_ms:
-        dom = ("unpack", unpack_ms / len(unpackers), unpack_bytes / len(unpackers))
-    else:
-        dom = ("pack", pack_ms / len(packers), pack_bytes / len(packers))
-    achieved = dom[2] / (dom[1] * 1e-3) / 1e9
-    traffic = measured_traffic(w.name, dom[0], dom[2])
+    # dominant copy launch: the kind of launch (side, state kind) taking the
+    # longest per step, at its per-launch average
+    groups = {}
+    for t, l in zip(launch_ms, launches):
+        g = groups.setdefault((l[0], l[1]), [0.0, 0, 0])
+        g[0] += t
+        g[1] += l[4]
+        g[2] += 1
+    (side, kind), (g_ms, g_bytes, g_n) = max(groups.items(), key=lambda kv: kv[1][0])
+    achieved = (g_bytes / g_n) / ((g_ms / g_n) * 1e-3) / 1e9
+    traffic = measured_traffic(w.name, side, g_bytes / g_n) if args.mode == "direct" and \
+        not args.identity else None
+    kernel = f"copy_kernel ({side}{'' if kind is None else f', kind {kind}'})"
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
+    share = ("all ranks" if w.mode == "full" else
+             f"pack of old rank {packers[0]}, unpack of new rank {unpackers[0]}")
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "src": f"TP{w.src.tp}xPP{w.src.pp}",
-                   "dst": f"TP{w.dst.tp}xPP{w.dst.pp}",
-                   "pairing": "identity" if args.identity else "migration sketch",
-                   "pack_ranks": packers,
-                   "unpack_ranks": unpackers, "alg_bytes_per_step": alg_bytes},
+                   "dst": f"TP{w.dst.tp}xPP{w.dst.pp}", "mode": args.mode,
+                   "pairing": {"identity": "identity", "sketch": "migration sketch",
+                               "coalesced": "coalesced (sketch + occupancy de-fragmentation)"}[pairing],
+                   "share": share, "pack_ranks": packers, "unpack_ranks": unpackers,
+                   "alg_bytes_per_step": alg_bytes},
         "frac_of_peak": round(value / PEAK_HBM_GBPS, 4),
         "pack_GBps": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1),
         "unpack_GBps": round(unpack_bytes / (unpack_ms * 1e-3) / 1e9, 1),
         "pack_ms": round(pack_ms, 4), "unpack_ms": round(unpack_ms, 4),
         "pack_bytes": pack_bytes, "unpack_bytes": unpack_bytes,
+        "launches_per_step": len(launches), "message_buffer_bytes": stage_bytes,
         "cost_matrix_us": round(cm_us, 2), "cost_matrix_cells": S * D,
-        "sketch_us": round(sketch_us, 1), "pairing": "identity" if args.identity else "sketch",
+        "sketch_us": round(sketch_us, 1), "pairing": pairing,
         "d2d_copy_GBps": round(d2d_gbps, 1), "plan_ms": round(plan_ms, 2),
-        "roofline": {"bound": "hbm", "kernel": f"copy_kernel ({dom[0]})",
+        "roofline": {"bound": "hbm", "kernel": kernel,
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic},
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle, one thread) ...")
-        out["cpu_baseline"] = cpu_baseline(w, args.identity)
+        out["cpu_baseline"] = cpu_baseline(w, pairing)
     print(json.dumps(out), flush=True)
 
 

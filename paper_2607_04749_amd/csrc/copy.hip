@@ -16,7 +16,9 @@
 // nothing is reused.  On MI355X this shape measured best of the ones tried
 // (deeper batches at low occupancy beat more resident waves with shallow
 // batches: the memory system is saturated and fewer, larger contiguous
-// request streams per CU use it better).
+// request streams per CU use it better).  A launch of a single state kind
+// (state chunking) also batches the shorter 2-byte rows 8 deep; a launch of
+// all four kinds does not, which measured faster there.
 #include <hip/hip_runtime.h>
 
 #include "copy_geom.hpp"
@@ -43,6 +45,8 @@ constexpr int kBatch2D = 4;    // vectors in flight per thread, strided rows
 
 // Copy nr rows of row_bytes bytes (16-byte aligned starts, row_bytes a
 // multiple of 16 when nr > 1) from src (row pitch sld bytes) to dst (pitch dld).
+// kSingle: the launch copies one state kind only.
+template <bool kSingle>
 __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64_t sld,
                                             char* __restrict__ dst, uint64_t dld, uint32_t nr,
                                             uint32_t row_bytes) {
@@ -60,6 +64,19 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
       for (int u = 0; u < kRowBatch; ++u)
         __builtin_nontemporal_store(
             v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
+    }
+    if (kSingle) {
+      for (; i + 7 * kCopyThreads < nv; i += 8 * kCopyThreads) {
+        u32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          v[u] = __builtin_nontemporal_load(
+              reinterpret_cast<const u32x4*>(src + uint64_t(i + u * kCopyThreads) * 16));
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          __builtin_nontemporal_store(
+              v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
+      }
     }
     for (; i < nv; i += kCopyThreads)
       __builtin_nontemporal_store(
@@ -104,7 +121,7 @@ __device__ __forceinline__ void copy_elems_2d(const E* __restrict__ src, uint64_
   }
 }
 
-template <bool kPack, int kKind>
+template <bool kPack, int kKind, bool kSingle>
 __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox& b, char* mbase,
                                                const TileGeom& g) {
   constexpr int es = kKind == 0 ? 2 : 4;
@@ -120,7 +137,7 @@ __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox&
   if (vec) {
     constexpr uint32_t vw = 16 / es;
     const uint32_t nvc = g.nr == 1 ? (g.nc / vw) * vw : g.nc;  // vector part of each row
-    copy_vec_2d(src, sld, dst, dld, g.nr, nvc * es);
+    copy_vec_2d<kSingle>(src, sld, dst, dld, g.nr, nvc * es);
     if (nvc < g.nc)
       copy_elems_2d<E>(reinterpret_cast<const E*>(src), sld / es, reinterpret_cast<E*>(dst),
                        dld / es, g.nr, nvc, g.nc);
@@ -135,7 +152,7 @@ __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox&
   }
 }
 
-template <bool kPack>
+template <bool kPack, bool kSingle>
 __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
   uint32_t t = blockIdx.x;
   if (t >= a.ntiles) return;
@@ -150,10 +167,10 @@ __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
     }
     const TileGeom g = tile_geom(b, t, next0);
     char* mbase = a.peer[b.peer];
-    if (a.kind_mask & 1) copy_tile_kind<kPack, 0>(a, b, mbase, g);
-    if (a.kind_mask & 2) copy_tile_kind<kPack, 1>(a, b, mbase, g);
-    if (a.kind_mask & 4) copy_tile_kind<kPack, 2>(a, b, mbase, g);
-    if (a.kind_mask & 8) copy_tile_kind<kPack, 3>(a, b, mbase, g);
+    if (a.kind_mask & 1) copy_tile_kind<kPack, 0, kSingle>(a, b, mbase, g);
+    if (a.kind_mask & 2) copy_tile_kind<kPack, 1, kSingle>(a, b, mbase, g);
+    if (a.kind_mask & 4) copy_tile_kind<kPack, 2, kSingle>(a, b, mbase, g);
+    if (a.kind_mask & 8) copy_tile_kind<kPack, 3, kSingle>(a, b, mbase, g);
   }
 }
 
@@ -174,10 +191,15 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   const uint32_t g = grid < ntiles ? grid : ntiles;
   // the dynamic LDS is not used by the kernel: it caps residency at one
   // workgroup per CU
-  if (pack)
-    hipLaunchKernelGGL(copy_kernel<true>, dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
+  const bool single = (kind_mask & (kind_mask - 1)) == 0;
+  if (pack && single)
+    hipLaunchKernelGGL((copy_kernel<true, true>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
+  else if (pack)
+    hipLaunchKernelGGL((copy_kernel<true, false>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
+  else if (single)
+    hipLaunchKernelGGL((copy_kernel<false, true>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
   else
-    hipLaunchKernelGGL(copy_kernel<false>, dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
+    hipLaunchKernelGGL((copy_kernel<false, false>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
   return hipGetLastError();
 }
 
