@@ -8,7 +8,10 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import DEV, ESIZE, alloc, emulate, equal, say, seeded_arenas
+from gpu_util import (DEV, ESIZE, alloc, emulate, equal, expected_dst, gather, say, seeded_arenas,
+                      to_dev)
+from helpers import empty_arenas as host_empty
+from helpers import host_arenas
 from micro import MICRO_MODELS, cfg_pairs
 from paper_2607_04749_amd import etc
 from paper_2607_04749_amd.workloads import WORKLOADS
@@ -76,10 +79,39 @@ def _compare_with_full(model, a, b, seed):
                 sec += npad * ESIZE[k]
 
 
+def _compare_with_oracle(model, a, b, seed):
+    """Chunked migration against the oracle directly: every target byte, and
+    every chunk message against the matching kind section of the oracle's
+    message."""
+    S, D = a.world, b.world
+    hs = host_arenas(model, a, range(S), seed)
+    hd = host_empty(model, b, range(D))
+    hb = {s: np.zeros(oracle.send_layout(model, a, b, s)[3], np.uint8) for s in range(S)}
+    oracle.migrate(model, a, b, hs, hd, hb)
+    plan = etc.etc_plan(model, a, b)
+    dst, chunks = chunked_migration(plan, to_dev(hs), range(D))
+    for d in range(D):
+        for k in range(4):
+            assert np.array_equal(dst[d][k].cpu().numpy(), hd[d][k]), f"target {d} kind {k}"
+    for s in range(S):
+        cnt, mb, dsp, _ = oracle.send_layout(model, a, b, s)
+        for d in range(D):
+            if not cnt[d]:
+                continue
+            npad = int(mb[d]) // 14
+            sec = int(dsp[d])
+            for k in range(4):
+                c, cd, _ = plan.chunk_layout(s, k)
+                got = chunks[k][s][int(cd[d]):int(cd[d]) + int(c[d])].cpu().numpy()
+                assert np.array_equal(got, hb[s][sec:sec + npad * ESIZE[k]]), f"chunk {s}->{d} kind {k}"
+                sec += npad * ESIZE[k]
+
+
 def test_tiny_chunked_equals_full():
     w = WORKLOADS["tiny-gpt"]
-    say("tiny-gpt chunked vs full")
+    say("tiny-gpt chunked vs full and vs the oracle")
     _compare_with_full(w.model, w.src, w.dst, w.seed)
+    _compare_with_oracle(w.model, w.src, w.dst, w.seed)
 
 
 @pytest.mark.parametrize("name", ["gpt", "ragged_llama"])
@@ -88,6 +120,54 @@ def test_micro_chunked_equals_full(name):
     for a, b in cfg_pairs(m)[::5]:
         say("micro chunked", name, a, "->", b)
         _compare_with_full(m, a, b, 31)
+        _compare_with_oracle(m, a, b, 31)
+
+
+def test_llama_70b_share_chunked():
+    """The 70B share kind by kind at real shape, in the launch configuration
+    the chunked benchmark times (the oracle's sketch pairing, which the
+    library's sketch also finds): the whole target against the seeded values,
+    and sampled chunk message elements against the oracle's serialization."""
+    w = WORKLOADS["llama-70b"]
+    pr = oracle.sketch(oracle.matrices(w.model, w.src, w.dst)["cost"])[0]
+    plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr)
+    s0, d0 = plan.process(w.pack_rank)
+    feeders = sorted({int(s) for s in np.nonzero(plan.recv_counts(d0))[0]} | {s0})
+    say("llama-70b chunked share: pack", s0, "unpack", d0, "sources", feeders)
+    src = seeded_arenas(w.model, w.src, feeders, w.seed)
+    rng = np.random.default_rng(70)
+    dst = [None] * 4
+    for k in range(4):
+        bufs = {}
+        for s in feeders:
+            bufs[s] = torch.zeros(max(plan.chunk_layout(s, k)[2], 256), dtype=torch.uint8, device=DEV)
+            etc.etc_pack_kind(plan, s, k, src[s][k], bufs[s])
+        msgs = []
+        for s in range(plan.S):
+            cnt, dsp, _ = plan.chunk_layout(s, k)
+            msgs.append(bufs[s].data_ptr() + int(dsp[d0]) if (s in bufs and cnt[d0]) else None)
+        dst[k] = torch.zeros(plan.arena_elems(etc.SIDE_DST, d0) * ESIZE[k], dtype=torch.uint8,
+                             device=DEV)
+        etc.etc_unpack_kind(plan, d0, k, msgs, dst[k])
+        torch.cuda.synchronize()
+        say("  kind", k, ": sampled chunk messages of source", s0)
+        cnt, dsp, _ = plan.chunk_layout(s0, k)
+        for d in np.nonzero(cnt)[0]:
+            npad = int(cnt[d]) // ESIZE[k]
+            pos = np.unique(rng.integers(0, npad, 4096, dtype=np.int64)).astype(np.uint64)
+            so = oracle.msg_origin(w.model, w.src, w.dst, s0, int(d), pos, pair=pr)
+            pad = so == np.uint64(2 ** 64 - 1)
+            got = gather(bufs[s0][int(dsp[d]):int(dsp[d]) + int(cnt[d])], k, pos)
+            want = np.zeros_like(got)
+            if (~pad).any():
+                want[~pad] = gather(src[s0][k], k, so[~pad])
+            np.testing.assert_array_equal(got, want, err_msg=f"chunk {s0}->{d} kind {k}")
+        del bufs
+        torch.cuda.empty_cache()
+    say("  full target vs seeded values")
+    exp = expected_dst(w.model, w.dst, d0, w.seed)
+    for k in range(4):
+        assert equal(dst[k], exp[k]), f"target {d0} kind {k}"
 
 
 def test_gpt_1_3b_chunked_eager_release_memory():
