@@ -129,6 +129,12 @@ def _ptr(x):
     return x.data_ptr()
 
 
+def last_error():
+    """Text of the calling thread's last error in the library ("" if none)."""
+    lib()
+    return _lib.etc_last_error().decode()
+
+
 def _stream(stream):
     if stream is None:
         import torch

@@ -78,6 +78,62 @@ def test_rank_bytes_closed_form(wl):
         assert held == rank_elems(w.model, w.src, s)
 
 
+def _copies(T, cfg, t):
+    """Copies of logical tensor t under cfg: TP copies of a replicated tensor,
+    two roles for the tied embedding when PP > 1."""
+    roles = 2 if (T[t]["tied_copy"] and cfg.pp > 1) else 1
+    return roles * (cfg.tp if T[t]["split"] == 0 else 1)
+
+
+@pytest.mark.parametrize("name", sorted(MICRO_MODELS))
+def test_route_rows_sum_to_source_bytes(name):
+    """Where no tensor changes its number of copies, every source copy serves
+    exactly one target copy, so each ROUTE row sums to the source rank's state
+    bytes (and each column to the target's), under the identity pairing and
+    under the sketch."""
+    m = MICRO_MODELS[name]
+    T = oracle.tensors(m)
+    n = 0
+    for a, b in cfg_pairs(m):
+        if any(_copies(T, a, t) != _copies(T, b, t) for t in range(len(T))):
+            continue
+        n += 1
+        C = oracle.matrices(m, a, b)["cost"]
+        for pair in (None, oracle.sketch(C)[0]):
+            R = oracle.matrices(m, a, b, pair=pair)["route"]
+            for s in range(a.world):
+                assert int(R[s].sum()) == 14 * rank_elems(m, a, s), (a, b, s)
+            for d in range(b.world):
+                assert int(R[:, d].sum()) == 14 * rank_elems(m, b, d)
+    assert n >= 3
+
+
+def test_route_rows_at_full_size():
+    """Llama-70B TP8xPP8 -> TP8xPP4 keeps every copy count: each ROUTE row is
+    the source's state bytes.  Llama-7B TP8 -> TP4 halves the copies of the
+    replicated norms (2 per layer plus the final norm: 65 x 4096 elements per
+    rank), so half of the sources send none of theirs: under the identity
+    pairing the targets take them from tp_s = tp_d (sources 0-3); under the
+    sketch each target's paired source keeps them (sources 0, 2, 4, 6).  The
+    other rows fall short by exactly those bytes."""
+    w = WORKLOADS["llama-70b"]
+    C = oracle.matrices(w.model, w.src, w.dst)["cost"]
+    for pair in (None, oracle.sketch(C)[0]):
+        R = oracle.matrices(w.model, w.src, w.dst, pair=pair)["route"]
+        for s in range(w.src.world):
+            assert int(R[s].sum()) == 14 * rank_elems(w.model, w.src, s)
+    w = WORKLOADS["llama-7b"]
+    repl = 14 * (2 * w.model.num_layers + 1) * w.model.hidden
+    assert repl == 3_727_360
+    C = oracle.matrices(w.model, w.src, w.dst)["cost"]
+    sk = oracle.sketch(C)[0]
+    for pair, senders in ((None, {0, 1, 2, 3}), (sk, {int(x) for x in sk})):
+        R = oracle.matrices(w.model, w.src, w.dst, pair=pair)["route"]
+        for s in range(w.src.world):
+            short = 0 if s in senders else repl
+            assert int(R[s].sum()) == 14 * rank_elems(w.model, w.src, s) - short, (pair, s)
+
+
 def test_tiny_totals():
     """Tiny GPT: 3,454,464 unique parameters (GPT count 12h^2+13h per layer
     with FFN 4h, plus embeddings and the final norm)."""
