@@ -18,11 +18,14 @@
  *     states of every workload type move together: bf16 parameter, fp32
  *     master, fp32 Adam m, fp32 Adam v (Sec. III-D).
  * This library is the data-parallel hot path of that migration on one GPU:
- *   etc_sketch      host: the migration sketch (pairing of new and old ranks)
- *   etc_plan        host: layouts, routing, message layout, tile tables
- *   etc_cost_matrix device: byte matrices over every (source, target) pair
- *   etc_pack        device: a source rank's shards -> one message per peer
- *   etc_unpack      device: received messages -> the target rank's shards
+ *   etc_sketch       host: the migration sketch (pairing of new and old ranks)
+ *   etc_plan         host: layouts, routing, message layout, tile tables
+ *   etc_plan_defrag  host: virtual rank allocator and the coalesced pairing
+ *   etc_cost_matrix  device: byte matrices over every (source, target) pair
+ *   etc_pack         device: a source rank's shards -> one message per peer
+ *   etc_unpack       device: received messages -> the target rank's shards
+ *   etc_pack_kind,   device: the same, one state kind at a time (state
+ *   etc_unpack_kind          chunking)
  * Moving messages between GPUs is the caller's business (a grouped
  * send/recv or all-to-all-v with the counts from etc_plan_send_layout).
  *
@@ -123,7 +126,7 @@ enum {
   ETC_ERR_INDIVISIBLE = -2, /* a dim the configuration splits does not divide     */
   ETC_ERR_RANK = -3,        /* rank out of range, or not built into this plan     */
   ETC_ERR_ALIGN = -4,       /* a device pointer is not 256-byte aligned           */
-  ETC_ERR_UNSUPPORTED = -5, /* dp != 1, too many peers, or a size limit exceeded  */
+  ETC_ERR_UNSUPPORTED = -5, /* a case outside the model family, too many peers or ranks, or a size limit */
   ETC_ERR_NOMEM = -6,       /* host or device allocation failed (etc_plan only)   */
   ETC_ERR_HIP = -7,         /* a HIP runtime call failed; see etc_last_error()    */
   ETC_ERR_UNRECOVERABLE = -8 /* needed data survives on no live source rank      */
