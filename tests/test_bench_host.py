@@ -1,0 +1,44 @@
+"""Host side of bench.py, no GPU: runs on more than one GPU are refused with a
+message, the committed HBM traffic record was taken on the copy kernel as it
+is now, and the CPU-baseline leg (the oracle on a bounded sample) runs."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from paper_2607_04749_amd.workloads import WORKLOADS  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_traffic_record_matches_the_kernel():
+    """Every record in the committed traffic file carries the hash of the
+    current copy-kernel sources, so bench.py reports it (a kernel change
+    without new counters would make it null)."""
+    with open(bench.TRAFFIC_FILE) as f:
+        rec = json.load(f)
+    assert set(rec) >= {"llama-70b", "llama-7b"}
+    for wl, kernels in rec.items():
+        for side, ent in kernels.items():
+            assert ent["kernel_hash"] == bench.kernel_hash(), (wl, side)
+            assert bench.measured_traffic(wl, side, 0) == ent["bytes_per_launch"]
+            # within 1 % of the algorithmic bytes: nothing is fetched twice
+            assert abs(ent["bytes_per_launch"] / ent["algorithmic_bytes"] - 1) < 0.01, (wl, side)
+
+
+@pytest.mark.parametrize("pairing", ["identity", "sketch"])
+def test_cpu_baseline_runs(pairing):
+    out = bench.cpu_baseline(WORKLOADS["tiny-gpt"], pairing)
+    assert out["kind"] == "oracle" and out["cores"] == 1 and out["unit"] == "GB/s"
+    assert out["value"] > 0 and "layer 0" in out["sample"]
