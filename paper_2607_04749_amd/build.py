@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libetc.so")
 BUILD_DIR = os.path.join(ROOT, "_build", "etc")
-SOURCES = ("plan.hip", "sketch.hip", "defrag.hip", "copy.hip", "cost.hip", "capi.hip")
+SOURCES = ("plan.hip", "tiles.hip", "sketch.hip", "defrag.hip", "copy.hip", "cost.hip", "capi.hip")
 
 # Packed fp32 ops are disabled for all device code (-packed-fp32-ops); the
 # host pass only warns that it does not know the feature.

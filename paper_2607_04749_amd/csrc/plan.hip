@@ -178,51 +178,6 @@ void check_model(const etc_model_desc& m) {
   if (m.flags & ~uint32_t(ETC_F_LAYERS_ONLY)) fail(ETC_ERR_INVALID_ARG, "unknown model flags");
 }
 
-// Cut one routed box into tiles and fill its copy descriptor.
-CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint64_t m_off,
-                 uint64_t msg_npad, int peer, bool pack, uint32_t tile0) {
-  CopyBox b{};
-  // a box whose rows are adjacent in the arena is one contiguous run
-  if (rows == 1 || cols == a_ld) {
-    cols = rows * cols;
-    rows = 1;
-    a_ld = cols;
-  }
-  if (cols > int64_t(UINT32_MAX) || rows > int64_t(UINT32_MAX) || a_ld > int64_t(UINT32_MAX))
-    fail(ETC_ERR_UNSUPPORTED, "a routed box exceeds 2^32 elements per row");
-  b.a_off = a_off;
-  b.m_off = m_off;
-  b.msg_npad = msg_npad;
-  b.a_ld = uint32_t(a_ld);
-  b.rows = uint32_t(rows);
-  b.cols = uint32_t(cols);
-  if (cols >= int64_t(kTileElems)) {
-    b.tc = kTileElems;
-    b.tr = 1;
-  } else {
-    b.tc = uint32_t(cols);
-    b.tr = uint32_t(std::max<int64_t>(1, std::min<int64_t>(rows, kTileElems / cols)));
-  }
-  b.ntc = uint32_t((cols + b.tc - 1) / b.tc);
-  b.tile0 = tile0;
-  b.peer = uint16_t(peer);
-  const uint64_t n = uint64_t(rows) * uint64_t(cols);
-  b.pad = pack ? uint8_t((8 - n % 8) % 8) : 0;
-  // 16-byte vectors: 8 elements of a 2-byte kind, 4 of a 4-byte kind.  The
-  // message side starts every box at a multiple of 8 elements.
-  auto ok = [&](uint64_t w) {
-    if (a_off % w) return false;
-    if (rows > 1 && (uint64_t(a_ld) % w || uint64_t(cols) % w)) return false;
-    return true;
-  };
-  b.vec = uint8_t((ok(8) ? 1 : 0) | (ok(4) ? 2 : 0));
-  return b;
-}
-
-uint32_t box_tiles(const CopyBox& b) {
-  const uint64_t ntr = (uint64_t(b.rows) + b.tr - 1) / b.tr;
-  return uint32_t(ntr * b.ntc);
-}
 
 }  // namespace
 
@@ -281,6 +236,21 @@ void build_host_plan(etc_plan_t& P) {
                                         " needed by target rank " + std::to_string(d));
     }
   }
+  // a copy launch addresses its peers' messages through a fixed table
+  std::vector<int> senders(D, 0);
+  for (int s = 0; s < S; ++s) {
+    int receivers = 0;
+    for (int d = 0; d < D; ++d)
+      if (!P.msg[size_t(s) * D + d].empty()) {
+        ++receivers;
+        ++senders[d];
+      }
+    if (receivers > ETC_MAX_PEERS)
+      fail(ETC_ERR_UNSUPPORTED, "source rank " + std::to_string(s) + " feeds more than ETC_MAX_PEERS targets");
+  }
+  for (int d = 0; d < D; ++d)
+    if (senders[d] > ETC_MAX_PEERS)
+      fail(ETC_ERR_UNSUPPORTED, "more than ETC_MAX_PEERS sources feed target rank " + std::to_string(d));
   P.msg_displ.assign(size_t(S) * D, 0);
   P.sendbuf_bytes.assign(S, 0);
   for (int s = 0; s < S; ++s) {
@@ -307,73 +277,6 @@ void build_host_plan(etc_plan_t& P) {
       P.chunk_bytes[i][s] = uint64_t(round_up(int64_t(cur), 256));
     }
   }
-}
-
-std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<int32_t>* peers,
-                                      uint64_t* bytes) {
-  const int D = P.dst.world();
-  std::vector<CopyBox> v;
-  uint32_t tiles = 0;
-  uint64_t moved = 0;
-  const RankLayout& L = P.src_layout[s];
-  peers->clear();
-  for (int d = 0; d < D; ++d) {
-    const size_t sd = size_t(s) * D + d;
-    if (P.msg[sd].empty()) continue;
-    const int slot = int(peers->size());
-    if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "one source feeds more than ETC_MAX_PEERS targets");
-    peers->push_back(d);
-    for (const auto& b : P.msg[sd]) {
-      const int role_s = role_on(P.route_tensors[b.tensor].src_stage, P.src.pp_of(s));
-      const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
-      const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
-      CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
-                           true, tiles);
-      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
-      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
-      tiles = uint32_t(nt);
-      moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
-      v.push_back(c);
-    }
-  }
-  CopyBox sentinel{};
-  sentinel.tile0 = tiles;
-  v.push_back(sentinel);
-  if (bytes) *bytes = moved;
-  return v;
-}
-
-std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,
-                                        uint64_t* bytes) {
-  const int S = P.src.world(), D = P.dst.world();
-  std::vector<CopyBox> v;
-  uint32_t tiles = 0;
-  uint64_t moved = 0;
-  const RankLayout& L = P.dst_layout[d];
-  peers->clear();
-  for (int s = 0; s < S; ++s) {
-    const size_t sd = size_t(s) * D + d;
-    if (P.msg[sd].empty()) continue;
-    const int slot = int(peers->size());
-    if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "more than ETC_MAX_PEERS sources feed one target");
-    peers->push_back(s);
-    for (const auto& b : P.msg[sd]) {
-      const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
-      const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
-      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
-                           false, tiles);
-      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
-      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
-      tiles = uint32_t(nt);
-      moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
-      v.push_back(c);
-    }
-  }
-  CopyBox sentinel{};
-  sentinel.tile0 = tiles;
-  v.push_back(sentinel);
-  if (bytes) *bytes = moved;
-  return v;
 }
 
 void build_route_tensors(etc_plan_t& P) {

@@ -95,6 +95,22 @@ def test_plan_errors(model, src, dst, code):
     assert etc.lib().etc_last_error()
 
 
+def test_peer_limit():
+    """A copy launch serves at most ETC_MAX_PEERS peers: 256 sources feeding
+    one target plan, 260 are refused up front, also for a host-only plan."""
+    from micro import layers_only
+    assert etc.MAX_PEERS == 256
+    p = etc.etc_plan(layers_only(256), Parallel(1, 256), Parallel(1, 1), flags=HOST)
+    assert int((p.recv_counts(0) > 0).sum()) == 256
+    p.free()
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan(layers_only(260), Parallel(1, 260), Parallel(1, 1), flags=HOST)
+    assert e.value.code == etc.ERR_UNSUPPORTED and "MAX_PEERS" in e.value.args[0]
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan(layers_only(260), Parallel(1, 1), Parallel(1, 260), flags=HOST)
+    assert e.value.code == etc.ERR_UNSUPPORTED
+
+
 def test_rank_and_flag_errors():
     w = WORKLOADS["tiny-gpt"]
     with pytest.raises(etc.EtcError) as e:

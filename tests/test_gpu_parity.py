@@ -117,6 +117,18 @@ def test_share_at_full_size(wl, pairing):
     share_run(w, plan, pair=pr)
 
 
+def test_max_peers_full_emulation():
+    """The most peers a launch serves: 256 sources feeding one target (every
+    message a different pipeline stage), and one source packing 256 messages;
+    byte for byte against the oracle, with the round trip."""
+    from micro import layers_only
+    m = layers_only(256)
+    say("256 sources -> 1 target")
+    full_compare(m, Parallel(1, 256), Parallel(1, 1), 59)
+    say("1 source -> 256 targets")
+    full_compare(m, Parallel(1, 1), Parallel(1, 256), 61, round_trip=False)
+
+
 def test_error_paths_on_device():
     w = WORKLOADS["tiny-gpt"]
     plan = etc.etc_plan(w.model, w.src, w.dst, rank=0)
