@@ -1,0 +1,59 @@
+"""Seeded random model shapes and configuration pairs (TP 1-6 including 3 and
+6, PP 1-4, DP 1-2, GPT and Llama, tied or untied, heads of width 1-4): the
+oracle's brute force equals its item form, every target receives exactly its
+bytes, and the library planner agrees with the oracle on layouts, message
+layouts and routing, under the identity pairing and under the sketch."""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import rank_elems
+from paper_2607_04749_amd import etc
+from paper_2607_04749_amd.workloads import Parallel
+from randcfg import cases
+
+HOST = etc.PLAN_HOST_ONLY
+CASES = cases(240)
+
+
+def sketch_pair(m, a, b):
+    C = oracle.matrices(m, a, b)["cost"]
+    pr, _ = oracle.sketch(C)
+    return np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(pr)],
+                    np.int32)
+
+
+def dp_bytes(m, cfg, r):
+    return 14 * rank_elems(m, Parallel(cfg.tp, cfg.pp), r % (cfg.tp * cfg.pp))
+
+
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_random_case(i):
+    m, a, b = CASES[i]
+    I = oracle.matrices(m, a, b)
+    if sum(dp_bytes(m, a, s) for s in range(a.world)) < 14 * 200_000:
+        B = oracle.matrices(m, a, b, brute=True)
+        for k in I:
+            np.testing.assert_array_equal(I[k], B[k], err_msg=k)
+    for d in range(b.world):
+        assert int(I["route"][:, d].sum()) == dp_bytes(m, b, d)
+    for pair in (None, sketch_pair(m, a, b)):
+        p = etc.etc_plan(m, a, b, flags=HOST, pair=pair)
+        R = oracle.matrices(m, a, b, pair=pair)["route"]
+        for side, cfg in ((etc.SIDE_SRC, a), (etc.SIDE_DST, b)):
+            for r in range(cfg.world):
+                want, elems = oracle.layout(m, cfg, r)
+                assert p.arena_elems(side, r) == elems
+                got = p.pieces(side, r)
+                assert [(x["tensor"], x["role"], x["r0"], x["r1"], x["c0"], x["c1"], x["off"]) for x in got] == \
+                       [(x["tensor"], x["role"], x["r0"], x["r1"], x["c0"], x["c1"], x["off"]) for x in want]
+        for s in range(a.world):
+            cnt, mb, dsp, tot = p.send_layout(s)
+            ocnt, opad, odsp, otot = oracle.send_layout(m, a, b, s, pair=pair)
+            np.testing.assert_array_equal(cnt, ocnt)
+            np.testing.assert_array_equal(mb, opad)
+            np.testing.assert_array_equal(dsp, odsp)
+            assert tot == otot
+        for d in range(b.world):
+            np.testing.assert_array_equal(p.recv_counts(d), R[:, d])
+        p.free()
