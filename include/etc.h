@@ -288,7 +288,8 @@ ETC_API int etc_cost_matrix(const etc_plan_t* plan, int which, uint64_t* d_out, 
  * k, device memory, read only) into send_buf (device, etc_plan_send_layout
  * total bytes): one contiguous message per target peer, the Send side of
  * Sec. III-D.  Every message byte is written (box padding is zero); other
- * bytes of send_buf are not touched.
+ * bytes of send_buf are not touched.  A source that routes nothing (a failed
+ * rank) returns ETC_OK at once, without reading any argument.
  * Errors: INVALID_ARG, RANK (src_rank's tables not built into the plan), ALIGN, HIP. */
 ETC_API int etc_pack(const etc_plan_t* plan, int src_rank, const void* const src_arena[4],
              void* send_buf, void* stream);
@@ -318,7 +319,8 @@ ETC_API int etc_plan_chunk_layout(const etc_plan_t* plan, int src_rank, int kind
                                   uint64_t* displs, uint64_t* total);
 
 /* Pack kind `kind` of source rank src_rank (src_arena: that kind's arena,
- * device, read only) into chunk_buf (device, chunk layout).  Errors as
+ * device, read only) into chunk_buf (device, chunk layout).  A source that
+ * routes nothing returns ETC_OK at once, as etc_pack does.  Errors as
  * etc_pack, and INVALID_ARG for a bad kind. */
 ETC_API int etc_pack_kind(const etc_plan_t* plan, int src_rank, int kind, const void* src_arena,
                           void* chunk_buf, void* stream);

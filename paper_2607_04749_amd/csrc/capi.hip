@@ -464,6 +464,7 @@ int etc_pack_kind(const etc_plan_t* P, int s, int kind, const void* src_arena, v
   if (s < 0 || s >= P->src.world()) return fail(ETC_ERR_RANK, "source rank out of range");
   const etc::CopyTable& t = P->pack_tab[s];
   if (!t.built) return fail(ETC_ERR_RANK, "source rank " + std::to_string(s) + " is not built into this plan");
+  if (t.ntiles == 0) return ETC_OK;  // routes nothing (e.g. a failed rank): nothing is read
   if (!src_arena || !chunk_buf) return fail(ETC_ERR_INVALID_ARG, "src_arena and chunk_buf must not be NULL");
   if (!aligned(src_arena, 256) || !aligned(chunk_buf, 256))
     return fail(ETC_ERR_ALIGN, "src_arena and chunk_buf must be 256-byte aligned");

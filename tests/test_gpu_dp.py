@@ -9,6 +9,7 @@ import torch
 import oracle
 from gpu_util import full_compare, say
 from micro import MICRO_MODELS
+from paper_2607_04749_amd import etc
 from paper_2607_04749_amd.workloads import WORKLOADS, Parallel as P
 
 pytestmark = pytest.mark.gpu
@@ -50,6 +51,14 @@ def test_micro_failed_ranks(failed):
     a, b = P(2, 1, 3), P(1, 2, 2)
     say("micro failed ranks", failed, a, "->", b)
     full_compare(m, a, b, 43, failed=failed)
+    # a failed source routes nothing: both pack calls return at once, reading
+    # none of their (here NULL) buffers
+    plan = etc.etc_plan(m, a, b, failed=failed)
+    for f in failed:
+        etc.etc_pack(plan, f, [None] * 4, None)
+        for k in range(4):
+            etc.etc_pack_kind(plan, f, k, None, None)
+    torch.cuda.synchronize()
 
 
 def test_tiny_gpt_dp_scale_out_and_failures():
