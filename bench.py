@@ -9,14 +9,17 @@ pairs rank d with rank d); the share is process 0's: the old rank it packs
 and the new rank it becomes.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
-                    [--identity] [--mode direct|chunked|coalesced]
+                    [--identity] [--mode direct|chunked|coalesced|refer]
 
 Modes: direct (default) packs and unpacks all four state kinds in one launch
 each; chunked moves one state kind at a time through per-kind chunk buffers
 (state chunking, Sec. III-D), four pack and four unpack launches per step;
 coalesced plans the migration with the coalesced pairing of occupancy
 de-fragmentation (Sec. III-E) and times the share of the first process that
-takes over a moved rank, which receives that rank's whole state.
+takes over a moved rank, which receives that rank's whole state; refer keeps
+the data a target's paired source holds on the GPU (Refer, Sec. III-D): it is
+copied arena to arena and travels in no message, so the step is the refer
+copy, the pack of what leaves and the unpack of what arrives.
 
 Prints one JSON line: value = algorithmic bytes of pack + unpack (each reads
 and writes its routed bytes) per step time, in GB/s; the roofline object is for
@@ -90,7 +93,7 @@ def oracle_pairing(w, pairing):
     return co, mv
 
 
-def cpu_baseline(w, pairing, layers=4):
+def cpu_baseline(w, pairing, layers=4, direct_refer=False):
     """The oracle (as it stands, one thread) on the tensors of a few layers of
     the same share (the first `layers` layers the target holds, about ten
     seconds on a current server core at the large shapes): materialize + cut
@@ -125,14 +128,21 @@ def cpu_baseline(w, pairing, layers=4):
         src[s] = [np.zeros(elems * e, np.uint8) for e in (2, 4, 4, 4)]
         synth.fill_host([p for p in pieces if t_lo <= p["tensor"] < t_hi], fc, src[s], w.seed)
     dst = {d0: [np.zeros(oracle.layout(m, b, d0)[1] * e, np.uint8) for e in (2, 4, 4, 4)]}
-    send = {s0: np.zeros(oracle.send_layout(m, a, b, s0, pair=pair)[3], np.uint8)}
-    sent = sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"]) for d in range(b.world)
-               for x in oracle.message(m, a, b, s0, d, pair=pair)[0] if x["tensor"] in sample)
-    got = sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"]) for s in range(a.world)
-              for x in oracle.message(m, a, b, s, d0, pair=pair)[0] if x["tensor"] in sample)
-    alg = 2 * sent + 2 * got
+    dr = direct_refer
+    send = {s0: np.zeros(oracle.send_layout(m, a, b, s0, pair=pair, direct_refer=dr)[3], np.uint8)}
+
+    def sample_bytes(s, d, direct):
+        return sum(14 * (x["r1"] - x["r0"]) * (x["c1"] - x["c0"])
+                   for x in oracle.message(m, a, b, s, d, pair=pair, direct_refer=direct)[0]
+                   if x["tensor"] in sample)
+
+    sent = sum(sample_bytes(s0, d, dr) for d in range(b.world))
+    got = sum(sample_bytes(s, d0, dr) for s in range(a.world))
+    home = int(pair[d0]) if pair is not None else (d0 if d0 < a.world else -1)
+    kept = sample_bytes(home, d0, False) if dr and home >= 0 else 0  # Refer: read and written once
+    alg = 2 * sent + 2 * got + 2 * kept
     t0 = time.perf_counter()
-    oracle.migrate(m, a, b, src, dst, send, t_lo, t_hi, pair=pair)
+    oracle.migrate(m, a, b, src, dst, send, t_lo, t_hi, pair=pair, direct_refer=dr)
     dt = time.perf_counter() - t0
     return {"value": round(alg / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"tensors of layers {held[0]}-{held[-1]} ({len(sample)} tensors): pack of source {s0} + "
@@ -148,7 +158,7 @@ def main():
     ap.add_argument("--workload", default="llama-70b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--identity", action="store_true", help="identity pairing instead of the sketch")
-    ap.add_argument("--mode", choices=("direct", "chunked", "coalesced"), default="direct")
+    ap.add_argument("--mode", choices=("direct", "chunked", "coalesced", "refer"), default="direct")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the migration; runs on more than one GPU "
@@ -184,7 +194,10 @@ def main():
             sys.exit(2)
         plan = etc.etc_plan(w.model, w.src, w.dst, pair=co)
     else:
-        plan = etc.etc_plan(w.model, w.src, w.dst, flags=0 if args.identity else etc.PLAN_SKETCH)
+        flags = 0 if args.identity else etc.PLAN_SKETCH
+        if args.mode == "refer":
+            flags |= etc.PLAN_DIRECT_REFER
+        plan = etc.etc_plan(w.model, w.src, w.dst, flags=flags)
     plan_ms = (time.perf_counter() - t0) * 1e3
     S, D = plan.S, plan.D
     if w.mode == "full":  # every source packs, every target unpacks
@@ -237,6 +250,15 @@ def main():
                     plan, d, k, msgs, dst[d][k]), nb))
         stage_bytes = sum(int(x.numel()) for x in buf.values())
     else:
+        if args.mode == "refer":  # the kept part of each target, from its paired source
+            home = plan.pairing()
+            for d in unpackers:
+                h = int(home[d])
+                if h >= 0 and plan.refer_bytes(d):
+                    if h not in src:
+                        raise SystemExit(f"paired source {h} of target {d} is not resident")
+                    launches.append(("refer", None, d, lambda d=d, h=h: etc.etc_refer(
+                        plan, d, src[h], dst[d]), 2 * plan.refer_bytes(d)))
         send = {s: torch.zeros(plan.send_layout(s)[3], dtype=torch.uint8, device=dev)
                 for s in resident}
         for s in resident:
@@ -244,6 +266,8 @@ def main():
                 etc.etc_pack(plan, s, src[s], send[s])
         layouts = {s: plan.send_layout(s) for s in resident}
         for s in packers:
+            if args.mode == "refer" and not int(layouts[s][0].sum()):
+                continue  # everything this source holds stays (Refer): no pack
             launches.append(("pack", None, s, lambda s=s: etc.etc_pack(plan, s, src[s], send[s]),
                              2 * int(layouts[s][0].sum())))
         for d in unpackers:
@@ -259,7 +283,8 @@ def main():
 
     pack_bytes = sum(l[4] for l in launches if l[0] == "pack")
     unpack_bytes = sum(l[4] for l in launches if l[0] == "unpack")
-    alg_bytes = pack_bytes + unpack_bytes
+    refer_bytes = sum(l[4] for l in launches if l[0] == "refer")
+    alg_bytes = pack_bytes + unpack_bytes + refer_bytes
 
     def step(ev=None):
         etc.etc_cost_matrix(plan, etc.CM_ROUTE, route)
@@ -287,6 +312,10 @@ def main():
                  for i in range(len(launches))]
     pack_ms = sum(t for t, l in zip(launch_ms, launches) if l[0] == "pack")
     unpack_ms = sum(t for t, l in zip(launch_ms, launches) if l[0] == "unpack")
+    refer_ms = sum(t for t, l in zip(launch_ms, launches) if l[0] == "refer")
+
+    def rate(nbytes, ms):
+        return round(nbytes / (ms * 1e-3) / 1e9, 1) if ms > 0 else None
 
     # cost matrices alone (events around a burst of launches)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -307,7 +336,7 @@ def main():
     sketch_us = sorted(ts)[2] * 1e6
 
     # practical ceiling: a plain device-to-device copy of half the unpack's bytes
-    nb = unpack_bytes // 2
+    nb = max(unpack_bytes, refer_bytes) // 2
     a_buf = torch.empty(nb, dtype=torch.uint8, device=dev)
     b_buf = torch.empty(nb, dtype=torch.uint8, device=dev)
     b_buf.copy_(a_buf)
@@ -344,11 +373,11 @@ def main():
                    "dst": f"TP{w.dst.tp}xPP{w.dst.pp}", "mode": args.mode,
                    "pairing": {"identity": "identity", "sketch": "migration sketch",
                                "coalesced": "coalesced (sketch + occupancy de-fragmentation)"}[pairing],
+                   "refer": "arena to arena (direct)" if args.mode == "refer" else "through a message",
                    "share": share, "pack_ranks": packers, "unpack_ranks": unpackers,
                    "alg_bytes_per_step": alg_bytes},
         "frac_of_peak": round(value / PEAK_HBM_GBPS, 4),
-        "pack_GBps": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1),
-        "unpack_GBps": round(unpack_bytes / (unpack_ms * 1e-3) / 1e9, 1),
+        "pack_GBps": rate(pack_bytes, pack_ms), "unpack_GBps": rate(unpack_bytes, unpack_ms),
         "pack_ms": round(pack_ms, 4), "unpack_ms": round(unpack_ms, 4),
         "pack_bytes": pack_bytes, "unpack_bytes": unpack_bytes,
         "launches_per_step": len(launches), "message_buffer_bytes": stage_bytes,
@@ -360,9 +389,13 @@ def main():
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic},
     }
+    if args.mode == "refer":
+        out["refer_GBps"] = rate(refer_bytes, refer_ms)
+        out["refer_ms"] = round(refer_ms, 4)
+        out["refer_bytes"] = refer_bytes
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle, one thread) ...")
-        out["cpu_baseline"] = cpu_baseline(w, pairing)
+        out["cpu_baseline"] = cpu_baseline(w, pairing, direct_refer=args.mode == "refer")
     print(json.dumps(out), flush=True)
 
 

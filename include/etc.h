@@ -117,8 +117,12 @@ enum { ETC_SIDE_SRC = 0, ETC_SIDE_DST = 1 };
 /* etc_plan flags */
 enum { ETC_PLAN_HOST_ONLY = 1, /* build host tables only: no device memory, no
                                   device calls allowed on this plan */
-       ETC_PLAN_SKETCH = 2     /* pair new and old ranks with the optimal
-                                  migration sketch (etc_sketch on COST) */ };
+       ETC_PLAN_SKETCH = 2,    /* pair new and old ranks with the optimal
+                                  migration sketch (etc_sketch on COST) */
+       ETC_PLAN_DIRECT_REFER = 4 /* the data a target's paired source keeps
+                                  (Refer, Sec. III-D) goes arena to arena
+                                  with etc_refer instead of through a
+                                  message: that message is empty */ };
 
 enum {
   ETC_OK = 0,
@@ -317,6 +321,22 @@ enum { ETC_MAX_PEERS = 256 };
  * any output may be NULL. */
 ETC_API int etc_plan_chunk_layout(const etc_plan_t* plan, int src_rank, int kind, uint64_t* counts,
                                   uint64_t* displs, uint64_t* total);
+
+/* Refer (Sec. III-D): data that target dst_rank's paired source already
+ * holds stays on that GPU.  With ETC_PLAN_DIRECT_REFER it is copied straight
+ * from the paired source's arenas (src_arena[k], read only) into dst_rank's
+ * (dst_arena[k]), all four kinds in one launch; the paired source's message
+ * to dst_rank is then empty, and etc_unpack writes the rest.  etc_refer and
+ * etc_unpack of one target write disjoint bytes, so they may run in either
+ * order or concurrently.  A target with no paired source, or a plan without
+ * the flag, has nothing to refer: ETC_OK at once.
+ * Errors: INVALID_ARG, RANK (dst_rank's tables not built into the plan), ALIGN, HIP. */
+ETC_API int etc_refer(const etc_plan_t* plan, int dst_rank, const void* const src_arena[4],
+                      void* const dst_arena[4], void* stream);
+
+/* Bytes (all four kinds) that etc_refer copies for dst_rank; 0 without
+ * ETC_PLAN_DIRECT_REFER or without a paired source. */
+ETC_API int etc_plan_refer_bytes(const etc_plan_t* plan, int dst_rank, uint64_t* bytes);
 
 /* Pack kind `kind` of source rank src_rank (src_arena: that kind's arena,
  * device, read only) into chunk_buf (device, chunk layout).  A source that

@@ -66,7 +66,7 @@ class MBox(ctypes.Structure):
 
 class Route(ctypes.Structure):
     _fields_ = [("pair", ctypes.c_void_p), ("failed", ctypes.c_void_p),
-                ("num_failed", ctypes.c_int32)]
+                ("num_failed", ctypes.c_int32), ("direct_refer", ctypes.c_int32)]
 
 
 class OracleError(RuntimeError):
@@ -122,14 +122,16 @@ def _ptr(a):
     return ctypes.c_void_p(a.ctypes.data) if a is not None else ctypes.c_void_p(0)
 
 
-def _route(pair, failed):
-    """orc_route for a pairing (new rank -> old rank or -1; None = identity)
-    and a list of failed old ranks.  Returns (keep-alive, pointer)."""
-    if pair is None and not failed:
+def _route(pair, failed, direct_refer=False):
+    """orc_route for a pairing (new rank -> old rank or -1; None = identity),
+    a list of failed old ranks and the direct-Refer switch.  Returns
+    (keep-alive, pointer)."""
+    if pair is None and not failed and not direct_refer:
         return None, ctypes.c_void_p(0)
     pa = None if pair is None else np.ascontiguousarray(pair, np.int32)
     fa = np.ascontiguousarray(failed if failed else [0], np.int32)
-    r = Route(None if pa is None else pa.ctypes.data, fa.ctypes.data, len(failed) if failed else 0)
+    r = Route(None if pa is None else pa.ctypes.data, fa.ctypes.data, len(failed) if failed else 0,
+              1 if direct_refer else 0)
     return (pa, fa, r), ctypes.cast(ctypes.pointer(r), ctypes.c_void_p)
 
 
@@ -174,7 +176,8 @@ def matrices(model, src, dst, brute=False, pair=None, failed=None):
     return dict(route=r, overlap=o, overlap_sharded=osh, cost=cst)
 
 
-def send_layout(model, src, dst, s, pair=None, failed=None):
+def send_layout(model, src, dst, s, pair=None, failed=None,
+                direct_refer=False):
     """(counts, padded, displs, total) in bytes for source s."""
     D = dst.world
     cnt = np.zeros(D, np.uint64)
@@ -182,17 +185,18 @@ def send_layout(model, src, dst, s, pair=None, failed=None):
     dsp = np.zeros(D, np.uint64)
     tot = ctypes.c_uint64()
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _route(pair, failed)
+    keep, pp = _route(pair, failed, direct_refer)
     _check(lib().orc_send_layout(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s,
                                  _ptr(cnt), _ptr(pad), _ptr(dsp), ctypes.byref(tot)), "send_layout")
     return cnt, pad, dsp, tot.value
 
 
-def message(model, src, dst, s, d, pair=None, failed=None):
+def message(model, src, dst, s, d, pair=None, failed=None,
+            direct_refer=False):
     """(boxes, npad): the boxes of message s->d in order, and the section length."""
     m, a, b = _m(model), _c(src), _c(dst)
     npad = ctypes.c_uint64()
-    keep, pp = _route(pair, failed)
+    keep, pp = _route(pair, failed, direct_refer)
     n = _check(lib().orc_message(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d, None,
                                  0, ctypes.byref(npad)), "message")
     arr = (MBox * max(n, 1))()
@@ -203,7 +207,7 @@ def message(model, src, dst, s, d, pair=None, failed=None):
 
 
 def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0, t_hi=-1,
-            pair=None, failed=None):
+            pair=None, failed=None, direct_refer=False):
     """Materialize-then-reslice.  src_arenas: {rank: [4 uint8 arrays]} (resident
     sources); dst_arenas: {rank: [4 uint8 arrays]} to fill; send_bufs:
     {rank: uint8 array} to fill with that source's messages."""
@@ -220,31 +224,33 @@ def migrate(model, src, dst, src_arenas, dst_arenas=None, send_bufs=None, t_lo=0
     for s, arr in (send_bufs or {}).items():
         sb[s] = arr.ctypes.data
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _route(pair, failed)
+    keep, pp = _route(pair, failed, direct_refer)
     _check(lib().orc_migrate(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp,
                              ctypes.cast(sa, ctypes.c_void_p), ctypes.cast(da, ctypes.c_void_p),
                              ctypes.cast(sb, ctypes.c_void_p), t_lo, t_hi), "migrate")
 
 
-def dst_origin(model, src, dst, d, offs, pair=None, failed=None):
+def dst_origin(model, src, dst, d, offs, pair=None, failed=None,
+               direct_refer=False):
     """(src_rank int32[n], src_off uint64[n]) for destination arena element offsets."""
     offs = np.ascontiguousarray(offs, np.uint64)
     rk = np.zeros(offs.size, np.int32)
     so = np.zeros(offs.size, np.uint64)
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _route(pair, failed)
+    keep, pp = _route(pair, failed, direct_refer)
     _check(lib().orc_dst_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, d,
                                 _ptr(offs), offs.size, _ptr(rk), _ptr(so)), "dst_origin")
     return rk, so
 
 
-def msg_origin(model, src, dst, s, d, pos, pair=None, failed=None):
+def msg_origin(model, src, dst, s, d, pos, pair=None, failed=None,
+               direct_refer=False):
     """Source-arena element offsets for element positions inside a kind section
     of message s->d (UINT64_MAX for padding)."""
     pos = np.ascontiguousarray(pos, np.uint64)
     so = np.zeros(pos.size, np.uint64)
     m, a, b = _m(model), _c(src), _c(dst)
-    keep, pp = _route(pair, failed)
+    keep, pp = _route(pair, failed, direct_refer)
     _check(lib().orc_msg_origin(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), pp, s, d,
                                 _ptr(pos), pos.size, _ptr(so)), "msg_origin")
     return so

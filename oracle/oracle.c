@@ -85,12 +85,15 @@ typedef struct {
 } orc_cfg;
 
 /* Routing inputs beyond the two configurations: the migration sketch
- * (pair[d] = old rank paired with new rank d, or -1; NULL = identity) and the
- * old ranks whose states are lost (failed[0..num_failed)). */
+ * (pair[d] = old rank paired with new rank d, or -1; NULL = identity), the
+ * old ranks whose states are lost (failed[0..num_failed)), and direct_refer:
+ * when non-zero, what a target's paired source keeps (Refer, Sec. III-D)
+ * travels in no message (it stays on that GPU), so that message is empty. */
 typedef struct {
   const int32_t* pair;
   const int32_t* failed;
   int32_t num_failed;
+  int32_t direct_refer;
 } orc_route;
 
 typedef struct {
@@ -313,6 +316,7 @@ typedef struct {
   orc_cfg src, dst;
   int S, D, nt;
   int32_t* home;  /* home[d]: source rank paired with target d (the same GPU), or -1 */
+  int direct_refer; /* Refer data travels in no message */
   char* failed;   /* failed[s]: source rank s lost its states */
   orc_tensor* T;
   int* ns;           /* pieces per source rank      */
@@ -377,6 +381,7 @@ static int ctx_init(ctx_t* x, const orc_model* m, const orc_cfg* src, const orc_
     ctx_free(x);
     return ORC_ENOMEM;
   }
+  x->direct_refer = route ? route->direct_refer : 0;
   for (int i = 0; route && i < route->num_failed; ++i) {
     if (route->failed[i] < 0 || route->failed[i] >= x->S) {
       ctx_free(x);
@@ -775,6 +780,11 @@ static int message_boxes(const ctx_t* x, int s, int d, orc_mbox* out, uint64_t* 
                          uint64_t* nelem) {
   int n = 0;
   uint64_t cur = 0, tot = 0;
+  if (x->direct_refer && x->home[d] == s) { /* kept on the paired GPU: no message */
+    if (npad) *npad = 0;
+    if (nelem) *nelem = 0;
+    return 0;
+  }
   for (int i = 0; i < x->nd[d]; ++i) {
     const orc_piece* q = &x->pd[d][i];
     const orc_tensor* t = &x->T[q->tensor];

@@ -114,6 +114,16 @@ int upload(etc_plan_t* P, int rank) {
   }
   for (int d = 0; d < D; ++d) {
     if (rank != ETC_ALL_RANKS && my_dst != d) continue;
+    CopyTable& t = P->refer_tab[d];
+    auto v = build_refer_boxes(*P, d, &t.bytes);
+    t.first = uint32_t(all.size());
+    t.nbox = uint32_t(v.size() - 1);
+    t.ntiles = v.back().tile0;
+    t.built = true;
+    all.insert(all.end(), v.begin(), v.end());
+  }
+  for (int d = 0; d < D; ++d) {
+    if (rank != ETC_ALL_RANKS && my_dst != d) continue;
     CopyTable& t = P->unpack_tab[d];
     auto v = build_unpack_boxes(*P, d, &t.peers, &t.bytes);
     t.first = uint32_t(all.size());
@@ -196,7 +206,8 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
   const int32_t* pair = opt->pair;
   const int rank = opt->rank;
   const uint32_t flags = opt->flags;
-  if (flags & ~uint32_t(ETC_PLAN_HOST_ONLY | ETC_PLAN_SKETCH)) return fail(ETC_ERR_INVALID_ARG, "unknown plan flags");
+  if (flags & ~uint32_t(ETC_PLAN_HOST_ONLY | ETC_PLAN_SKETCH | ETC_PLAN_DIRECT_REFER))
+    return fail(ETC_ERR_INVALID_ARG, "unknown plan flags");
   if (pair && (flags & ETC_PLAN_SKETCH)) return fail(ETC_ERR_INVALID_ARG, "pass a pairing or ETC_PLAN_SKETCH, not both");
   if (opt->num_failed < 0 || (opt->num_failed > 0 && !opt->failed))
     return fail(ETC_ERR_INVALID_ARG, "bad failed-rank list");
@@ -248,6 +259,7 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
     etc::build_host_plan(*P);
     P->pack_tab.resize(S);
     P->unpack_tab.resize(D);
+    P->refer_tab.resize(D);
     if (!(flags & ETC_PLAN_HOST_ONLY)) {
       const int rc = upload(P.get(), rank);
       if (rc != ETC_OK) {
@@ -410,7 +422,7 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
   for (size_t i = 0; i < t.peers.size(); ++i)
     peers[i] = static_cast<char*>(send_buf) + P->msg_displ[size_t(s) * D + t.peers[i]];
   hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 0xFu, true, arenas, peers,
+                                  P->copy_lds_reserve, 0xFu, etc::kMsgSections, arenas, peers,
                                   int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
   return ETC_OK;
@@ -433,7 +445,7 @@ int etc_unpack(const etc_plan_t* P, int d, const void* const* msg, void* const d
     peers[i] = const_cast<void*>(p);
   }
   hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 0xFu, true, dst_arena, peers,
+                                  P->copy_lds_reserve, 0xFu, etc::kMsgSections, dst_arena, peers,
                                   int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
   return ETC_OK;
@@ -476,7 +488,7 @@ int etc_pack_kind(const etc_plan_t* P, int s, int kind, const void* src_arena, v
   for (size_t j = 0; j < t.peers.size(); ++j)
     peers[j] = static_cast<char*>(chunk_buf) + P->chunk_displ[i][size_t(s) * D + t.peers[j]];
   hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 1u << kind, false, arenas, peers,
+                                  P->copy_lds_reserve, 1u << kind, etc::kMsgOneKind, arenas, peers,
                                   int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
   return ETC_OK;
@@ -504,9 +516,36 @@ int etc_unpack_kind(const etc_plan_t* P, int d, int kind, const void* const* msg
   void* arenas[4] = {nullptr, nullptr, nullptr, nullptr};
   arenas[kind] = dst_arena;
   hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 1u << kind, false, arenas, peers,
+                                  P->copy_lds_reserve, 1u << kind, etc::kMsgOneKind, arenas, peers,
                                   int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
+  return ETC_OK;
+}
+
+int etc_refer(const etc_plan_t* P, int d, const void* const src_arena[4], void* const dst_arena[4],
+              void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
+  const etc::CopyTable& t = P->refer_tab[d];
+  if (!t.built) return fail(ETC_ERR_RANK, "target rank " + std::to_string(d) + " is not built into this plan");
+  if (t.ntiles == 0) return ETC_OK;  // nothing kept by a paired source
+  if ((rc = check_arenas(src_arena, "src_arena"))) return rc;
+  if ((rc = check_arenas(const_cast<const void* const*>(dst_arena), "dst_arena"))) return rc;
+  void* sources[4];
+  for (int k = 0; k < 4; ++k) sources[k] = const_cast<void*>(src_arena[k]);
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
+                                  P->copy_lds_reserve, 0xFu, etc::kMsgArenas, dst_arena, sources, 4,
+                                  static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "refer launch");
+  return ETC_OK;
+}
+
+int etc_plan_refer_bytes(const etc_plan_t* P, int d, uint64_t* bytes) {
+  int rc = check_side_rank(P, ETC_SIDE_DST, d);
+  if (rc) return rc;
+  if (!bytes) return fail(ETC_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = P->refer_elems[size_t(d)] * 14;
   return ETC_OK;
 }
 

@@ -2,7 +2,8 @@
 //
 // Pure data movement, HBM bound: each launch copies a list of routed boxes
 // between a rank's four state arenas (strided rows) and message sections
-// (contiguous rows), for all four state kinds.  Boxes are pre-cut on the host
+// (contiguous rows), for all four state kinds, or (Refer) straight from a
+// source rank's arenas into a target rank's.  Boxes are pre-cut on the host
 // into uniform tiles of kTileElems elements per kind.
 //
 // Launch shape: a persistent grid of one 256-thread workgroup per CU (the
@@ -35,9 +36,9 @@ struct CopyArgs {
   uint32_t nbox;
   uint32_t ntiles;
   uint32_t kind_mask;  // kinds to copy (bit k)
-  uint32_t sectioned;  // 1: messages hold four kind sections; 0: one kind
+  uint32_t mode;       // MsgMode: what peer[] points at
   char* arena[4];
-  char* peer[ETC_MAX_PEERS];  // start of each peer's message
+  char* peer[ETC_MAX_PEERS];  // start of each peer's message (kMsgArenas: source arena of kind k)
 };
 
 constexpr int kRowBatch = 16;  // vectors in flight per thread, contiguous rows
@@ -127,12 +128,14 @@ __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox&
   constexpr int es = kKind == 0 ? 2 : 4;
   using E = typename std::conditional<es == 2, uint16_t, uint32_t>::type;
   char* A = a.arena[kKind] + tile_arena_elem(b, g) * es;
-  char* Mb = mbase + (a.sectioned ? section_byte(b.msg_npad, kKind) : 0);  // this kind's section
+  // this kind's section of the message, or (Refer) the source arena of this kind
+  char* Mb = a.mode == kMsgArenas ? a.peer[kKind]
+                                  : mbase + (a.mode == kMsgSections ? section_byte(b.msg_npad, kKind) : 0);
   char* M = Mb + tile_msg_elem(b, g) * es;
   const char* src = kPack ? A : M;
   char* dst = kPack ? M : A;
-  const uint64_t sld = uint64_t(kPack ? b.a_ld : b.cols) * es;
-  const uint64_t dld = uint64_t(kPack ? b.cols : b.a_ld) * es;
+  const uint64_t sld = (kPack ? uint64_t(b.a_ld) : b.m_ld) * es;
+  const uint64_t dld = (kPack ? b.m_ld : uint64_t(b.a_ld)) * es;
   const bool vec = (b.vec >> (es == 2 ? 0 : 1)) & 1;
   if (vec) {
     constexpr uint32_t vw = 16 / es;
@@ -177,7 +180,7 @@ __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
 }  // namespace
 
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, bool sectioned,
+                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, MsgMode mode,
                        void* const arena[4], void* const* peers, int npeers, hipStream_t stream) {
   if (ntiles == 0 || kind_mask == 0) return hipSuccess;
   CopyArgs a{};
@@ -185,7 +188,7 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   a.nbox = nbox;
   a.ntiles = ntiles;
   a.kind_mask = kind_mask;
-  a.sectioned = sectioned ? 1u : 0u;
+  a.mode = mode;
   for (int k = 0; k < 4; ++k) a.arena[k] = static_cast<char*>(arena[k]);
   for (int p = 0; p < npeers; ++p) a.peer[p] = static_cast<char*>(peers[p]);
   const uint32_t g = grid < ntiles ? grid : ntiles;

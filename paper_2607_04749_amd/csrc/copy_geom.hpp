@@ -46,7 +46,7 @@ __host__ __device__ inline uint64_t tile_arena_elem(const CopyBox& b, const Tile
   return b.a_off + uint64_t(g.r0) * b.a_ld + g.c0;
 }
 __host__ __device__ inline uint64_t tile_msg_elem(const CopyBox& b, const TileGeom& g) {
-  return b.m_off + uint64_t(g.r0) * b.cols + g.c0;
+  return b.m_off + uint64_t(g.r0) * b.m_ld + g.c0;
 }
 
 // Byte offset of kind k's section inside a message of npad elements per section.

@@ -77,7 +77,7 @@ struct CopyBox {
   uint64_t a_off;     // arena element offset of the box's first element
   uint64_t m_off;     // element offset inside each kind section of the message
   uint64_t msg_npad;  // elements per kind section of that message
-  uint64_t reserved;
+  uint64_t m_ld;      // message-side row stride (elements): cols, or a source arena's row stride
   uint32_t a_ld;      // arena row stride, elements
   uint32_t rows, cols;  // box shape; contiguous boxes are collapsed to one row
   uint32_t tr, tc;    // tile shape (rows x cols)
@@ -103,11 +103,17 @@ constexpr uint32_t kTileElems = 16384;  // nominal tile: 16384 elements per kind
 constexpr int kCopyThreads = 256;
 constexpr int kCmThreads = 256;
 
+// What the message side of a copy launch is.
+enum MsgMode : uint32_t {
+  kMsgOneKind = 0,   // one kind per message (chunk format)
+  kMsgSections = 1,  // four kind sections per message (full format)
+  kMsgArenas = 2,    // no message: peers[k] is a source arena of kind k (Refer)
+};
+
 // kernel launchers (copy.hip, cost.hip)
-// kind_mask: kinds to copy (bit k); sectioned: messages hold all four kind
-// sections (full format) rather than one kind (chunk format)
+// kind_mask: kinds to copy (bit k)
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, bool sectioned,
+                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, MsgMode mode,
                        void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
 // Routing context of a plan: both grids and the failed source ranks (bitmap,
 // nullptr when none).  Device copies point at device memory.
@@ -140,6 +146,10 @@ struct etc_plan_s {
     uint64_t moff;
   };
   std::vector<std::vector<MsgBox>> msg;
+  // [d]: boxes that d's paired source keeps (Refer), copied arena to arena by
+  // etc_refer when the plan has ETC_PLAN_DIRECT_REFER; no message carries them
+  std::vector<std::vector<MsgBox>> refer;
+  std::vector<uint64_t> refer_elems;
   std::vector<uint64_t> msg_elems;  // routed elements
   std::vector<uint64_t> msg_npad;   // padded elements per kind section
   std::vector<uint64_t> msg_displ;  // byte displacement in the sender's buffer
@@ -158,5 +168,5 @@ struct etc_plan_s {
   int32_t* d_home = nullptr;  // device copy of home (D entries)
   uint32_t* d_failed = nullptr;  // device copy of failed_bits
   etc::CopyBox* d_boxes = nullptr;
-  std::vector<etc::CopyTable> pack_tab, unpack_tab;
+  std::vector<etc::CopyTable> pack_tab, unpack_tab, refer_tab;
 };

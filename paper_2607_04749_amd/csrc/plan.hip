@@ -202,6 +202,9 @@ void build_host_plan(etc_plan_t& P) {
   P.msg.assign(size_t(S) * D, {});
   P.msg_elems.assign(size_t(S) * D, 0);
   P.msg_npad.assign(size_t(S) * D, 0);
+  P.refer.assign(D, {});
+  P.refer_elems.assign(D, 0);
+  const bool direct_refer = (P.flags & ETC_PLAN_DIRECT_REFER) != 0;
   for (int d = 0; d < D; ++d) {
     for (const Piece& q : P.dst_layout[d].pieces) {
       const RouteTensor& rt = P.route_tensors[q.tensor];
@@ -224,12 +227,17 @@ void build_host_plan(etc_plan_t& P) {
           b.c1 = x.hi;
         }
         const uint64_t n = uint64_t((b.r1 - b.r0) * (b.c1 - b.c0));
+        got += n;
+        if (direct_refer && s == P.home[d]) {  // kept by the paired source: no message
+          P.refer[d].push_back(b);
+          P.refer_elems[d] += n;
+          continue;
+        }
         const size_t sd = size_t(s) * D + d;
         b.moff = P.msg_npad[sd];
         P.msg_npad[sd] += uint64_t(round_up(int64_t(n), 8));
         P.msg_elems[sd] += n;
         P.msg[sd].push_back(b);
-        got += n;
       }
       if (got != q.elems())
         fail(ETC_ERR_UNRECOVERABLE, "no live source rank holds part of " + P.tensors[q.tensor].name +

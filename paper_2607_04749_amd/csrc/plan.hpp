@@ -38,5 +38,7 @@ std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<in
                                       uint64_t* bytes);
 std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,
                                         uint64_t* bytes);
+// Refer boxes of target d: its paired source's arenas -> its arenas
+std::vector<CopyBox> build_refer_boxes(const etc_plan_t& P, int d, uint64_t* bytes);
 
 }  // namespace etc

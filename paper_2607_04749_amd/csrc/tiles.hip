@@ -18,20 +18,25 @@ namespace {
 void fail(int code, const std::string& msg) { throw PlanError(code, msg); }
 
 // Cut one routed box into tiles and fill its copy descriptor.
+// m_ld: row stride on the message side (cols for a message, whose boxes are
+// row-major; a source arena's row stride for a Refer box).
 CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint64_t m_off,
-                 uint64_t msg_npad, int peer, bool pack, uint32_t tile0) {
+                 uint64_t msg_npad, int peer, bool pack, uint32_t tile0, int64_t m_ld) {
   CopyBox b{};
-  // a box whose rows are adjacent in the arena is one contiguous run
-  if (rows == 1 || cols == a_ld) {
+  // a box whose rows are adjacent on both sides is one contiguous run
+  if (rows == 1 || (cols == a_ld && cols == m_ld)) {
     cols = rows * cols;
     rows = 1;
     a_ld = cols;
+    m_ld = cols;
   }
-  if (cols > int64_t(UINT32_MAX) || rows > int64_t(UINT32_MAX) || a_ld > int64_t(UINT32_MAX))
+  if (cols > int64_t(UINT32_MAX) || rows > int64_t(UINT32_MAX) || a_ld > int64_t(UINT32_MAX) ||
+      m_ld > int64_t(UINT32_MAX))
     fail(ETC_ERR_UNSUPPORTED, "a routed box exceeds 2^32 elements per row");
   b.a_off = a_off;
   b.m_off = m_off;
   b.msg_npad = msg_npad;
+  b.m_ld = uint64_t(m_ld);
   b.a_ld = uint32_t(a_ld);
   b.rows = uint32_t(rows);
   b.cols = uint32_t(cols);
@@ -50,8 +55,8 @@ CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint6
   // 16-byte vectors: 8 elements of a 2-byte kind, 4 of a 4-byte kind.  The
   // message side starts every box at a multiple of 8 elements.
   auto ok = [&](uint64_t w) {
-    if (a_off % w) return false;
-    if (rows > 1 && (uint64_t(a_ld) % w || uint64_t(cols) % w)) return false;
+    if (a_off % w || m_off % w) return false;
+    if (rows > 1 && (uint64_t(a_ld) % w || uint64_t(cols) % w || uint64_t(m_ld) % w)) return false;
     return true;
   };
   b.vec = uint8_t((ok(8) ? 1 : 0) | (ok(4) ? 2 : 0));
@@ -84,7 +89,7 @@ std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<in
       const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
       const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
       CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
-                           true, tiles);
+                           true, tiles, b.c1 - b.c0);
       const uint64_t nt = uint64_t(tiles) + box_tiles(c);
       if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
       tiles = uint32_t(nt);
@@ -117,7 +122,36 @@ std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<
       const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
       const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
       CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
-                           false, tiles);
+                           false, tiles, b.c1 - b.c0);
+      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
+      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
+      tiles = uint32_t(nt);
+      moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
+      v.push_back(c);
+    }
+  }
+  CopyBox sentinel{};
+  sentinel.tile0 = tiles;
+  v.push_back(sentinel);
+  if (bytes) *bytes = moved;
+  return v;
+}
+
+std::vector<CopyBox> build_refer_boxes(const etc_plan_t& P, int d, uint64_t* bytes) {
+  std::vector<CopyBox> v;
+  uint32_t tiles = 0;
+  uint64_t moved = 0;
+  const int h = P.home[d];
+  if (h >= 0) {
+    const RankLayout& L = P.dst_layout[d];
+    const RankLayout& H = P.src_layout[h];
+    for (const auto& b : P.refer[d]) {
+      const int role_s = role_on(P.route_tensors[b.tensor].src_stage, P.src.pp_of(h));
+      const Piece& p = H.pieces[H.piece_of_tensor[role_s][b.tensor]];
+      const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
+      const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
+      const uint64_t s_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
+      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, s_off, 0, 0, false, tiles, p.ld());
       const uint64_t nt = uint64_t(tiles) + box_tiles(c);
       if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
       tiles = uint32_t(nt);

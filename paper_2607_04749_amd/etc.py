@@ -25,6 +25,7 @@ ALL_RANKS = -1
 SIDE_SRC, SIDE_DST = 0, 1
 PLAN_HOST_ONLY = 1
 PLAN_SKETCH = 2
+PLAN_DIRECT_REFER = 4
 OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP = \
     0, -1, -2, -3, -4, -5, -6, -7
 ERR_UNRECOVERABLE = -8
@@ -82,6 +83,8 @@ def _load():
                            ctypes.POINTER(vp)]
     L.etc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
     L.etc_plan_pairing.argtypes = [vp, vp]
+    L.etc_refer.argtypes = [vp, ctypes.c_int, vp, vp, vp]
+    L.etc_plan_refer_bytes.argtypes = [vp, ctypes.c_int, u64p]
     L.etc_plan_defrag.argtypes = [vp, ctypes.c_int, vp, vp, i32p, vp]
     L.etc_plan_process.argtypes = [vp, ctypes.c_int, i32p, i32p]
     L.etc_plan_free.argtypes = [vp]
@@ -211,6 +214,12 @@ class Plan:
                "etc_plan_send_layout")
         return cnt, mb, dsp, tot.value
 
+    def refer_bytes(self, d):
+        """Bytes etc_refer copies for target d (ETC_PLAN_DIRECT_REFER plans)."""
+        n = ctypes.c_uint64()
+        _check(_lib.etc_plan_refer_bytes(self.handle, d, ctypes.byref(n)), "etc_plan_refer_bytes")
+        return n.value
+
     def pairing(self):
         """pair[d] = old rank paired with new rank d, or -1."""
         pr = np.zeros(self.D, np.int32)
@@ -298,6 +307,14 @@ def etc_unpack(plan, dst_rank, msgs, dst_arenas, stream=None):
     arr = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
     _check(_lib.etc_unpack(plan.handle, dst_rank, ctypes.cast(m, ctypes.c_void_p),
                            ctypes.cast(arr, ctypes.c_void_p), _stream(stream)), "etc_unpack")
+
+
+def etc_refer(plan, dst_rank, src_arenas, dst_arenas, stream=None):
+    """Refer: dst_rank's kept data from its paired source's arenas into its own."""
+    src = (ctypes.c_void_p * 4)(*[_ptr(x) for x in src_arenas])
+    dst = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
+    _check(_lib.etc_refer(plan.handle, dst_rank, ctypes.cast(src, ctypes.c_void_p),
+                          ctypes.cast(dst, ctypes.c_void_p), _stream(stream)), "etc_refer")
 
 
 def etc_pack_kind(plan, src_rank, kind, src_arena, chunk_buf, stream=None):

@@ -124,11 +124,14 @@ def emulate(plan, src_arenas, dst_ranks, dst_alloc, skip=()):
             msgs.append(send[s].data_ptr() + int(dsp[d]) if cnt[d] else None)
         dst[d] = dst_alloc(d)
         etc.etc_unpack(plan, d, msgs, dst[d])
+        h = int(plan.pairing()[d])
+        if plan.refer_bytes(d):  # ETC_PLAN_DIRECT_REFER: the kept part, arena to arena
+            etc.etc_refer(plan, d, src_arenas[h], dst[d])
     torch.cuda.synchronize()
     return send, dst
 
 
-def full_compare(model, src, dst, seed, pair=None, round_trip=True, failed=None):
+def full_compare(model, src, dst, seed, pair=None, round_trip=True, failed=None, direct_refer=False):
     """Full emulation on the GPU vs the oracle, every byte.  Failed sources'
     arenas hold garbage and are never packed."""
     from helpers import empty_arenas as host_empty
@@ -140,10 +143,12 @@ def full_compare(model, src, dst, seed, pair=None, round_trip=True, failed=None)
         for arr in hs[f]:
             arr[:] = 0xA5
     hd = host_empty(model, dst, range(D))
-    hb = {s: np.zeros(oracle.send_layout(model, src, dst, s, pair=pair, failed=failed)[3], np.uint8)
+    hb = {s: np.zeros(oracle.send_layout(model, src, dst, s, pair=pair, failed=failed,
+                                         direct_refer=direct_refer)[3], np.uint8)
           for s in range(S)}
-    oracle.migrate(model, src, dst, hs, hd, hb, pair=pair, failed=failed)
-    plan = etc.etc_plan(model, src, dst, pair=pair, failed=failed)
+    oracle.migrate(model, src, dst, hs, hd, hb, pair=pair, failed=failed, direct_refer=direct_refer)
+    plan = etc.etc_plan(model, src, dst, pair=pair, failed=failed,
+                        flags=etc.PLAN_DIRECT_REFER if direct_refer else 0)
     check_matrices(plan, model, src, dst, pair, failed)
     ds = to_dev(hs)
     send, dd = emulate(plan, ds, range(D), lambda d: alloc(plan.arena_elems(etc.SIDE_DST, d)),

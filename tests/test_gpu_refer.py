@@ -1,0 +1,87 @@
+"""Direct Refer on the GPU (Sec. III-D: what a target's paired source already
+holds stays on that GPU): with ETC_PLAN_DIRECT_REFER the kept part is copied
+arena to arena by etc_refer and the paired source's message is empty.
+Targets and every message byte against the oracle under the same switch;
+the 70B share at real shape against the seeded values."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import (DEV, alloc, equal, expected_dst, full_compare, sampled_origin_check, say,
+                      seeded_arenas)
+from micro import MICRO_MODELS, cfg_pairs
+from paper_2607_04749_amd import etc
+from paper_2607_04749_amd.workloads import WORKLOADS
+from randcfg import cases
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _sketch(m, a, b):
+    C = oracle.matrices(m, a, b)["cost"]
+    sk, _ = oracle.sketch(C)
+    return np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)],
+                    np.int32)
+
+
+@pytest.mark.parametrize("name", ["gpt", "llama_gqa", "ragged_llama"])
+def test_micro_direct_refer(name):
+    m = MICRO_MODELS[name]
+    for a, b in cfg_pairs(m)[::3]:
+        for pr in (None, _sketch(m, a, b)):
+            say("micro direct refer", name, a, "->", b, "pair", None if pr is None else list(pr))
+            full_compare(m, a, b, 67, pair=pr, round_trip=False, direct_refer=True)
+
+
+def test_tiny_direct_refer():
+    w = WORKLOADS["tiny-gpt"]
+    say("tiny-gpt direct refer")
+    full_compare(w.model, w.src, w.dst, w.seed, pair=_sketch(w.model, w.src, w.dst),
+                 round_trip=False, direct_refer=True)
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_direct_refer(i):
+    m, a, b = cases(12)[i]
+    say("random direct refer", i, m, a, "->", b)
+    full_compare(m, a, b, 0xEF + i, pair=_sketch(m, a, b), round_trip=False, direct_refer=True)
+
+
+def test_llama_70b_share_direct_refer():
+    """Process 0 keeps half of its new rank's state (its own layers) and
+    receives the other half from one peer: refer + unpack at real shape."""
+    w = WORKLOADS["llama-70b"]
+    pr = _sketch(w.model, w.src, w.dst)
+    plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr, flags=etc.PLAN_DIRECT_REFER)
+    s0, d0 = plan.process(w.pack_rank)
+    feeders = sorted(int(s) for s in np.nonzero(plan.recv_counts(d0))[0])
+    say("llama-70b direct refer: process", w.pack_rank, "old", s0, "new", d0, "feeders", feeders,
+        "refer GB", plan.refer_bytes(d0) / 1e9)
+    assert s0 not in feeders and plan.refer_bytes(d0) > 0
+    src = seeded_arenas(w.model, w.src, sorted(set(feeders) | {s0}), w.seed)
+    send = {}
+    for s in feeders:
+        send[s] = torch.zeros(plan.send_layout(s)[3], dtype=torch.uint8, device=DEV)
+        etc.etc_pack(plan, s, src[s], send[s])
+    msgs = [send[s].data_ptr() + int(plan.send_layout(s)[2][d0]) if s in send else None
+            for s in range(plan.S)]
+    dst = alloc(plan.arena_elems(etc.SIDE_DST, d0))
+    etc.etc_refer(plan, d0, src[s0], dst)
+    etc.etc_unpack(plan, d0, msgs, dst)
+    torch.cuda.synchronize()
+    say("  sampled origins")
+    sampled_origin_check(w.model, w.src, w.dst, d0, dst, src, pair=pr)
+    del send
+    torch.cuda.empty_cache()
+    say("  full target vs seeded values")
+    exp = expected_dst(w.model, w.dst, d0, w.seed)
+    for k in range(4):
+        assert equal(dst[k], exp[k]), f"target {d0} kind {k}"

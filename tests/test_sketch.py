@@ -206,3 +206,51 @@ def test_bad_pairings_rejected():
     assert e.value.code == etc.ERR_INVALID_ARG
     with pytest.raises(oracle.OracleError):
         oracle.matrices(w.model, w.src, w.dst, pair=[0, 0, 1, 2])
+
+
+@pytest.mark.parametrize("wl", sorted(WORKLOADS))
+def test_direct_refer_layouts(wl):
+    """ETC_PLAN_DIRECT_REFER: a target's paired source sends it no message;
+    what it keeps (Refer) is exactly OVERLAP[home][d], the paper's shared
+    workload of the pair, and with the messages it makes up the target's
+    state.  Message layouts equal the oracle's under the same switch."""
+    w = WORKLOADS[wl]
+    m, a, b = w.model, w.src, w.dst
+    M = oracle.matrices(m, a, b)
+    pr = oracle.sketch(M["cost"])[0]
+    for pair in (None, pr):
+        p = etc.etc_plan(m, a, b, flags=HOST | etc.PLAN_DIRECT_REFER, pair=pair)
+        home = p.pairing()
+        for s in range(a.world):
+            cnt, mb, dsp, tot = p.send_layout(s)
+            ocnt, opad, odsp, otot = oracle.send_layout(m, a, b, s, pair=pair, direct_refer=True)
+            np.testing.assert_array_equal(cnt, ocnt)
+            np.testing.assert_array_equal(mb, opad)
+            np.testing.assert_array_equal(dsp, odsp)
+            assert tot == otot
+        Mp = oracle.matrices(m, a, b, pair=pair)
+        for d in range(b.world):
+            recv = p.recv_counts(d)
+            kept = p.refer_bytes(d)
+            if home[d] >= 0:
+                assert recv[home[d]] == 0
+                assert kept == int(M["overlap"][home[d], d]) == int(Mp["route"][home[d], d])
+            else:
+                assert kept == 0
+            assert int(recv.sum()) + kept == 14 * rank_elems(m, b, d)
+        p.free()
+
+
+def test_direct_refer_micro_matches_oracle():
+    for name in ("gpt", "llama_gqa", "ragged_gpt"):
+        m = MICRO_MODELS[name]
+        for a, b in cfg_pairs(m)[::3]:
+            pr = oracle.sketch(oracle.matrices(m, a, b)["cost"])[0]
+            p = etc.etc_plan(m, a, b, flags=HOST | etc.PLAN_DIRECT_REFER, pair=pr)
+            for s in range(a.world):
+                ocnt, opad, odsp, otot = oracle.send_layout(m, a, b, s, pair=pr, direct_refer=True)
+                cnt, mb, dsp, tot = p.send_layout(s)
+                np.testing.assert_array_equal(mb, opad)
+                np.testing.assert_array_equal(dsp, odsp)
+                assert tot == otot
+            p.free()
