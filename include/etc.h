@@ -334,6 +334,11 @@ ETC_API int etc_plan_chunk_layout(const etc_plan_t* plan, int src_rank, int kind
 ETC_API int etc_refer(const etc_plan_t* plan, int dst_rank, const void* const src_arena[4],
                       void* const dst_arena[4], void* stream);
 
+/* etc_refer for one state kind (state chunking): src_arena and dst_arena are
+ * that kind's arenas.  Errors as etc_refer, and INVALID_ARG for a bad kind. */
+ETC_API int etc_refer_kind(const etc_plan_t* plan, int dst_rank, int kind, const void* src_arena,
+                           void* dst_arena, void* stream);
+
 /* Bytes (all four kinds) that etc_refer copies for dst_rank; 0 without
  * ETC_PLAN_DIRECT_REFER or without a paired source. */
 ETC_API int etc_plan_refer_bytes(const etc_plan_t* plan, int dst_rank, uint64_t* bytes);

@@ -541,6 +541,29 @@ int etc_refer(const etc_plan_t* P, int d, const void* const src_arena[4], void* 
   return ETC_OK;
 }
 
+int etc_refer_kind(const etc_plan_t* P, int d, int kind, const void* src_arena, void* dst_arena,
+                   void* stream) {
+  int rc = check_device_plan(P);
+  if (rc) return rc;
+  if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
+  if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
+  const etc::CopyTable& t = P->refer_tab[d];
+  if (!t.built) return fail(ETC_ERR_RANK, "target rank " + std::to_string(d) + " is not built into this plan");
+  if (t.ntiles == 0) return ETC_OK;
+  if (!src_arena || !dst_arena) return fail(ETC_ERR_INVALID_ARG, "src_arena and dst_arena must not be NULL");
+  if (!aligned(src_arena, 256) || !aligned(dst_arena, 256))
+    return fail(ETC_ERR_ALIGN, "src_arena and dst_arena must be 256-byte aligned");
+  void* arenas[4] = {nullptr, nullptr, nullptr, nullptr};
+  void* sources[4] = {nullptr, nullptr, nullptr, nullptr};
+  arenas[kind] = dst_arena;
+  sources[kind] = const_cast<void*>(src_arena);
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
+                                  P->copy_lds_reserve, 1u << kind, etc::kMsgArenas, arenas, sources, 4,
+                                  static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "refer launch");
+  return ETC_OK;
+}
+
 int etc_plan_refer_bytes(const etc_plan_t* P, int d, uint64_t* bytes) {
   int rc = check_side_rank(P, ETC_SIDE_DST, d);
   if (rc) return rc;

@@ -84,6 +84,7 @@ def _load():
     L.etc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
     L.etc_plan_pairing.argtypes = [vp, vp]
     L.etc_refer.argtypes = [vp, ctypes.c_int, vp, vp, vp]
+    L.etc_refer_kind.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, vp]
     L.etc_plan_refer_bytes.argtypes = [vp, ctypes.c_int, u64p]
     L.etc_plan_defrag.argtypes = [vp, ctypes.c_int, vp, vp, i32p, vp]
     L.etc_plan_process.argtypes = [vp, ctypes.c_int, i32p, i32p]
@@ -315,6 +316,12 @@ def etc_refer(plan, dst_rank, src_arenas, dst_arenas, stream=None):
     dst = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
     _check(_lib.etc_refer(plan.handle, dst_rank, ctypes.cast(src, ctypes.c_void_p),
                           ctypes.cast(dst, ctypes.c_void_p), _stream(stream)), "etc_refer")
+
+
+def etc_refer_kind(plan, dst_rank, kind, src_arena, dst_arena, stream=None):
+    """etc_refer for one state kind (that kind's arenas)."""
+    _check(_lib.etc_refer_kind(plan.handle, dst_rank, kind, _ptr(src_arena), _ptr(dst_arena),
+                               _stream(stream)), "etc_refer_kind")
 
 
 def etc_pack_kind(plan, src_rank, kind, src_arena, chunk_buf, stream=None):

@@ -85,3 +85,53 @@ def test_llama_70b_share_direct_refer():
     exp = expected_dst(w.model, w.dst, d0, w.seed)
     for k in range(4):
         assert equal(dst[k], exp[k]), f"target {d0} kind {k}"
+
+
+def test_chunked_direct_refer():
+    """State chunking and direct Refer together: kind by kind, pack, refer
+    and unpack give the oracle's targets and chunk messages (the home chunk
+    message is empty)."""
+    w = WORKLOADS["tiny-gpt"]
+    m, a, b = w.model, w.src, w.dst
+    pr = _sketch(m, a, b)
+    from helpers import empty_arenas as host_empty
+    from helpers import host_arenas
+    from gpu_util import ESIZE, to_dev
+    S, D = a.world, b.world
+    hs = host_arenas(m, a, range(S), w.seed)
+    hd = host_empty(m, b, range(D))
+    hb = {s: np.zeros(oracle.send_layout(m, a, b, s, pair=pr, direct_refer=True)[3], np.uint8)
+          for s in range(S)}
+    oracle.migrate(m, a, b, hs, hd, hb, pair=pr, direct_refer=True)
+    plan = etc.etc_plan(m, a, b, pair=pr, flags=etc.PLAN_DIRECT_REFER)
+    home = plan.pairing()
+    ds = to_dev(hs)
+    dst = {d: [None] * 4 for d in range(D)}
+    for k in range(4):
+        bufs = {}
+        for s in range(S):
+            bufs[s] = torch.zeros(max(plan.chunk_layout(s, k)[2], 256), dtype=torch.uint8, device=DEV)
+            etc.etc_pack_kind(plan, s, k, ds[s][k], bufs[s])
+        for d in range(D):
+            msgs = []
+            for s in range(S):
+                cnt, dsp, _ = plan.chunk_layout(s, k)
+                msgs.append(bufs[s].data_ptr() + int(dsp[d]) if cnt[d] else None)
+            dst[d][k] = torch.zeros(plan.arena_elems(etc.SIDE_DST, d) * ESIZE[k], dtype=torch.uint8,
+                                    device=DEV)
+            etc.etc_unpack_kind(plan, d, k, msgs, dst[d][k])
+            if home[d] >= 0:
+                etc.etc_refer_kind(plan, d, k, ds[int(home[d])][k], dst[d][k])
+        torch.cuda.synchronize()
+        for s in range(S):  # chunk k of s->d is section k of the oracle's message
+            cnt, mb, dsp, _ = oracle.send_layout(m, a, b, s, pair=pr, direct_refer=True)
+            c, cd, _ = plan.chunk_layout(s, k)
+            for d in np.nonzero(cnt)[0]:
+                npad = int(mb[d]) // 14
+                sec = int(dsp[d]) + sum(npad * ESIZE[j] for j in range(k))
+                got = bufs[s][int(cd[d]):int(cd[d]) + int(c[d])].cpu().numpy()
+                assert np.array_equal(got, hb[s][sec:sec + npad * ESIZE[k]]), f"chunk {s}->{d} kind {k}"
+            assert all(c[d] == 0 for d in range(D) if home[d] == s)
+    for d in range(D):
+        for k in range(4):
+            assert np.array_equal(dst[d][k].cpu().numpy(), hd[d][k]), f"target {d} kind {k}"
