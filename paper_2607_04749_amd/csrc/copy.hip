@@ -8,8 +8,9 @@
 //
 // Launch shape: a persistent grid of one 256-thread workgroup per CU (the
 // launcher reserves just over half of a CU's LDS per workgroup, so no second
-// workgroup can become resident), walking tiles interleaved (tile t goes to
-// workgroup t mod grid), so the whole GPU sweeps the buffers front to back.
+// workgroup can become resident), walking tiles interleaved round by round
+// over the grid, each XCD taking a contiguous run of every round
+// (first_tile), so the whole GPU sweeps the buffers front to back.
 // A tile's descriptor is uniform across the workgroup (scalar loads).
 // Within a tile, each thread moves 16-byte vectors in batches: 16 loads in
 // flight, then the 16 stores, for contiguous rows (a workgroup streams 64 KB
@@ -157,7 +158,7 @@ __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox&
 
 template <bool kPack, bool kSingle>
 __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
-  uint32_t t = blockIdx.x;
+  uint32_t t = first_tile(blockIdx.x, gridDim.x);
   if (t >= a.ntiles) return;
   uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
   CopyBox b = a.boxes[bi];

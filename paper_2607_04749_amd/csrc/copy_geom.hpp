@@ -12,6 +12,16 @@
 
 namespace etc {
 
+constexpr uint32_t kXcds = 8;  // MI355X: 8 accelerator complex dies, 32 CUs each
+
+// First tile of workgroup `block` in a grid of `grid` workgroups; later ones
+// follow every `grid` tiles.  Workgroups are dispatched round-robin over the
+// XCDs, so block mod 8 is its XCD; within each round of `grid` tiles the
+// workgroups of one XCD take a contiguous run of grid / 8 tiles.
+__host__ __device__ inline uint32_t first_tile(uint32_t block, uint32_t grid) {
+  return grid % kXcds == 0 ? (block % kXcds) * (grid / kXcds) + block / kXcds : block;
+}
+
 // Index of the box holding tile t: the last box with tile0 <= t.
 __host__ __device__ inline uint32_t box_of_tile(const CopyBox* boxes, uint32_t nbox, uint32_t t) {
   uint32_t lo = 0, hi = nbox;

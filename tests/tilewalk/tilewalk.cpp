@@ -48,7 +48,7 @@ static void replay(const std::vector<CopyBox>& v, bool pack, bool sectioned, uin
   if (ntiles == 0) return;
   G = G < ntiles ? G : ntiles;
   for (uint32_t bid = 0; bid < G; ++bid) {
-    uint32_t t = bid;
+    uint32_t t = first_tile(bid, G);
     uint32_t bi = box_of_tile(v.data(), nbox, t);
     CopyBox b = v[bi]; uint32_t next0 = v[bi + 1].tile0;
     for (; t < ntiles; t += G) {
