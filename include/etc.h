@@ -214,6 +214,9 @@ typedef struct {
  * that process's pack and unpack, or for every rank with ETC_ALL_RANKS, and
  * copied to the current device, which the plan is then bound to.  With
  * ETC_PLAN_HOST_ONLY no device memory is touched.
+ * A routed run of contiguous elements may exceed 2^32 elements (it is copied
+ * in pieces of 2^31); no tensor size limit applies beyond the int32 fields of
+ * etc_model_desc.
  * On success *out owns host and device memory until etc_plan_free.
  * Errors: INVALID_ARG (also a bad pairing or failed list), INDIVISIBLE,
  * UNSUPPORTED (GPT with GQA, more than 65536 ranks, a rank exchanging messages

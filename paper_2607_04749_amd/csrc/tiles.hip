@@ -17,22 +17,20 @@ namespace {
 
 void fail(int code, const std::string& msg) { throw PlanError(code, msg); }
 
-// Cut one routed box into tiles and fill its copy descriptor.
+// Longest row of a copy descriptor: a contiguous run longer than 2^32 - 1
+// elements is cut into rows of this many elements plus a one-row remainder.
+// A multiple of 8 and of kTileElems, so vector alignment and tile boundaries
+// carry over to the pieces.
+constexpr int64_t kMaxRunElems = int64_t(1) << 31;
+
+// Fill the copy descriptor of one box with its tiles starting at tile0.
 // m_ld: row stride on the message side (cols for a message, whose boxes are
 // row-major; a source arena's row stride for a Refer box).
 CopyBox make_box(uint64_t a_off, int64_t a_ld, int64_t rows, int64_t cols, uint64_t m_off,
                  uint64_t msg_npad, int peer, bool pack, uint32_t tile0, int64_t m_ld) {
+  if (cols > int64_t(UINT32_MAX) || rows > int64_t(UINT32_MAX) || a_ld > int64_t(UINT32_MAX))
+    fail(ETC_ERR_UNSUPPORTED, "a strided routed box exceeds 2^32 - 1 rows or elements per row");
   CopyBox b{};
-  // a box whose rows are adjacent on both sides is one contiguous run
-  if (rows == 1 || (cols == a_ld && cols == m_ld)) {
-    cols = rows * cols;
-    rows = 1;
-    a_ld = cols;
-    m_ld = cols;
-  }
-  if (cols > int64_t(UINT32_MAX) || rows > int64_t(UINT32_MAX) || a_ld > int64_t(UINT32_MAX) ||
-      m_ld > int64_t(UINT32_MAX))
-    fail(ETC_ERR_UNSUPPORTED, "a routed box exceeds 2^32 elements per row");
   b.a_off = a_off;
   b.m_off = m_off;
   b.msg_npad = msg_npad;
@@ -68,6 +66,34 @@ uint32_t box_tiles(const CopyBox& b) {
   return uint32_t(ntr * b.ntc);
 }
 
+// Append the descriptors of one routed box (rows x cols elements, arena row
+// stride a_ld, message-side row stride m_ld) to a launch of `tiles` tiles so far.
+// A box whose rows are adjacent on both sides is one contiguous run and is
+// copied as such: as one row, or, beyond kMaxRunElems, as full rows of
+// kMaxRunElems elements and a remainder row (the pack pads only after the last).
+void add_box(std::vector<CopyBox>& v, uint32_t& tiles, uint64_t a_off, int64_t a_ld, int64_t rows,
+             int64_t cols, uint64_t m_off, uint64_t msg_npad, int peer, bool pack, int64_t m_ld) {
+  auto push = [&](const CopyBox& c) {
+    const uint64_t nt = uint64_t(tiles) + box_tiles(c);
+    if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
+    tiles = uint32_t(nt);
+    v.push_back(c);
+  };
+  if (rows == 1 || (cols == a_ld && cols == m_ld)) {
+    const int64_t n = rows * cols;
+    const int64_t full = n > int64_t(UINT32_MAX) ? n / kMaxRunElems : 0;
+    if (full > 0)
+      push(make_box(a_off, kMaxRunElems, full, kMaxRunElems, m_off, msg_npad, peer, false, tiles,
+                    kMaxRunElems));
+    const int64_t done = full * kMaxRunElems, rest = n - done;
+    if (rest > 0)
+      push(make_box(a_off + uint64_t(done), rest, 1, rest, m_off + uint64_t(done), msg_npad, peer, pack,
+                    tiles, rest));
+    return;
+  }
+  push(make_box(a_off, a_ld, rows, cols, m_off, msg_npad, peer, pack, tiles, m_ld));
+}
+
 }  // namespace
 
 std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<int32_t>* peers,
@@ -88,13 +114,9 @@ std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<in
       const int role_s = role_on(P.route_tensors[b.tensor].src_stage, P.src.pp_of(s));
       const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
       const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
-      CopyBox c = make_box(a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
-                           true, tiles, b.c1 - b.c0);
-      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
-      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
-      tiles = uint32_t(nt);
+      add_box(v, tiles, a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot, true,
+              b.c1 - b.c0);
       moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
-      v.push_back(c);
     }
   }
   CopyBox sentinel{};
@@ -121,13 +143,9 @@ std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<
     for (const auto& b : P.msg[sd]) {
       const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
       const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
-      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot,
-                           false, tiles, b.c1 - b.c0);
-      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
-      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
-      tiles = uint32_t(nt);
+      add_box(v, tiles, a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot, false,
+              b.c1 - b.c0);
       moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
-      v.push_back(c);
     }
   }
   CopyBox sentinel{};
@@ -151,12 +169,8 @@ std::vector<CopyBox> build_refer_boxes(const etc_plan_t& P, int d, uint64_t* byt
       const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
       const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
       const uint64_t s_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
-      CopyBox c = make_box(a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, s_off, 0, 0, false, tiles, p.ld());
-      const uint64_t nt = uint64_t(tiles) + box_tiles(c);
-      if (nt > UINT32_MAX) fail(ETC_ERR_UNSUPPORTED, "too many tiles for one launch");
-      tiles = uint32_t(nt);
+      add_box(v, tiles, a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, s_off, 0, 0, false, p.ld());
       moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
-      v.push_back(c);
     }
   }
   CopyBox sentinel{};

@@ -124,3 +124,17 @@ def test_random_configurations(tilewalk):
         jobs.append(_args(m, a, b, 256, False, "identity"))
         jobs.append(_args(m, a, b, 256, True, _oracle_sketch(m, a, b)))
     _run_all(tilewalk, jobs)
+
+
+def test_contiguous_run_beyond_2_32_elements(tilewalk):
+    """GPT, hidden 17, vocab 2^28 + 1: the embedding is one contiguous run of
+    4,563,402,769 elements, cut into 2^31-element rows and a ragged remainder
+    (the pack pads 7 elements after it)."""
+    from paper_2607_04749_amd.workloads import GPT, ModelShape
+    m = ModelShape(GPT, 2, 17, 1, 1, 8, 2 ** 28 + 1, 0, 1)
+    jobs = []
+    for b in (P(1, 1), P(1, 2)):
+        for grid in (256, 7):
+            for refer in (False, True):
+                jobs.append(_args(m, P(1, 1), b, grid, refer, "identity"))
+    _run_all(tilewalk, jobs)
