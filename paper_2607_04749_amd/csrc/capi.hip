@@ -235,10 +235,7 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
     etc::build_route_tensors(*P);
     P->home.assign(D, -1);
     if (flags & ETC_PLAN_SKETCH) {
-      const std::vector<uint64_t> cost = etc::host_cost_matrix(*P);
-      etc::solve_sketch(cost.data(), D, S, P->home.data());
-      for (int d = 0; d < D; ++d)  // a pair across replicas or with a dead rank is no pair
-        if (P->home[d] >= 0 && cost[size_t(d) * S + P->home[d]] >= uint64_t(ETC_COST_INF)) P->home[d] = -1;
+      etc::sketch_pairing(*P, dead);
     } else if (pair) {
       std::vector<char> taken(S, 0);
       for (int d = 0; d < D; ++d) {

@@ -179,6 +179,34 @@ void check_model(const etc_model_desc& m) {
 }
 
 
+// Source ranks that may send part of tensor t to target d, ascending: a
+// superset of those for which routed_span is not empty.  They are the paired
+// source, and the ranks on the tensor's stages whose TP shard overlaps d's in
+// the replicas that may serve d: replica rep_d mod DP_src alone when no rank
+// failed (it always holds the tensor), every replica otherwise (failover).
+void candidate_senders(const RouteTensor& t, int d, int home, const RouteCtx& c,
+                       std::vector<int>* out) {
+  out->clear();
+  const int rd = d % (c.tpd * c.ppd);
+  const int tp_d = rd % c.tpd, rep_d = d / (c.tpd * c.ppd);
+  int tp_lo = 0, tp_hi = c.tps;  // source TP ranks [tp_lo, tp_hi)
+  if (t.split != kRepl) {
+    const Span need = shard_span(t, tp_d, c.tpd);
+    const int64_t w = split_extent(t) / c.tps;
+    tp_lo = int(need.lo / w);
+    tp_hi = int((need.hi + w - 1) / w);
+  }
+  const int pt = c.tps * c.pps;
+  const int rep_lo = c.failed ? 0 : rep_d % c.dps, rep_hi = c.failed ? c.dps : rep_lo + 1;
+  for (int rep = rep_lo; rep < rep_hi; ++rep)
+    for (int r = 0; r < 2; ++r)
+      if (t.src_stage[r] >= 0)
+        for (int tp = tp_lo; tp < tp_hi; ++tp) out->push_back(rep * pt + t.src_stage[r] * c.tps + tp);
+  if (home >= 0) out->push_back(home);
+  std::sort(out->begin(), out->end());
+  out->erase(std::unique(out->begin(), out->end()), out->end());
+}
+
 }  // namespace
 
 PlanError::PlanError(int c, std::string m) : std::runtime_error(std::move(m)), code(c) {}
@@ -205,11 +233,13 @@ void build_host_plan(etc_plan_t& P) {
   P.refer.assign(D, {});
   P.refer_elems.assign(D, 0);
   const bool direct_refer = (P.flags & ETC_PLAN_DIRECT_REFER) != 0;
+  std::vector<int> cand;
   for (int d = 0; d < D; ++d) {
     for (const Piece& q : P.dst_layout[d].pieces) {
       const RouteTensor& rt = P.route_tensors[q.tensor];
       uint64_t got = 0;
-      for (int s = 0; s < S; ++s) {
+      candidate_senders(rt, d, P.home[d], ctx, &cand);
+      for (const int s : cand) {
         const Span x = routed_span(rt, s, d, P.home[d], ctx);
         if (x.len() == 0) continue;
         etc_plan_s::MsgBox b{};
@@ -316,20 +346,17 @@ RouteCtx host_route_ctx(const etc_plan_t& P) {
                   P.failed_bits.empty() ? nullptr : P.failed_bits.data()};
 }
 
-std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P) {
-  // COST[d][s] = bytes(d) - OVERLAP[s][d], the same interval arithmetic as
-  // the cost kernel, on the host (feeds the migration sketch at plan time);
-  // ETC_COST_INF across data-parallel replicas and to failed ranks
-  const int S = P.src.world(), D = P.dst.world();
-  const RouteCtx ctx = host_route_ctx(P);
-  std::vector<uint64_t> cost(size_t(D) * S, 0);
-  for (int d = 0; d < D; ++d) {
+// COST of one data-parallel replica pair (Sec. III-B, bytes): rows are the
+// target ranks of a replica, columns the source ranks of one, COST[d][s] =
+// bytes(d) - OVERLAP[s][d] with the interval arithmetic of the cost kernel.
+// Every replica pair has this block, since a rank's workload depends only on
+// its TP and PP coordinates.
+std::vector<uint64_t> host_replica_cost(const etc_plan_t& P) {
+  const int Sr = P.src.replica_size(), Dr = P.dst.replica_size();
+  std::vector<uint64_t> cost(size_t(Dr) * Sr, 0);
+  for (int d = 0; d < Dr; ++d) {
     const int pp_d = P.dst.pp_of(d), tp_d = P.dst.tp_of(d);
-    for (int s = 0; s < S; ++s) {
-      if (rank_dead(ctx, s) || P.src.replica(s) != P.dst.replica(d)) {
-        cost[size_t(d) * S + s] = ETC_COST_INF;
-        continue;
-      }
+    for (int s = 0; s < Sr; ++s) {
       const int pp_s = P.src.pp_of(s), tp_s = P.src.tp_of(s);
       uint64_t need = 0, ov = 0;
       for (const RouteTensor& t : P.route_tensors) {
@@ -341,10 +368,51 @@ std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P) {
         const Span x{std::max(have.lo, want.lo), std::min(have.hi, want.hi)};
         ov += uint64_t(x.len() * unit_elems(t));
       }
-      cost[size_t(d) * S + s] = (need - ov) * 14;
+      cost[size_t(d) * Sr + s] = (need - ov) * 14;
     }
   }
   return cost;
+}
+
+// The migration sketch (Algorithm 1) with DP isolation (Sec. III-C).  COST is
+// infinite across replicas and to failed ranks, so the zero-padded assignment
+// over all ranks splits into one assignment per replica that both grids have
+// (target replica r with source replica r).  Its pairs of finite cost are the
+// pairs of finite cost of the assignment over the whole matrix: every
+// cross-replica pair costs the same, and the number of them is forced.
+// Replicas without failed ranks share one solution.  Pairs of infinite cost
+// (a failed rank) are dropped; targets of replicas the source grid lacks stay
+// unpaired.
+void sketch_pairing(etc_plan_t& P, const std::vector<char>& dead) {
+  const int Sr = P.src.replica_size(), Dr = P.dst.replica_size();
+  const int reps = std::min(P.src.dp, P.dst.dp);
+  P.home.assign(P.dst.world(), -1);
+  const std::vector<uint64_t> base = host_replica_cost(P);
+  std::vector<int32_t> base_pair, pair(Dr);
+  std::vector<uint64_t> cost;
+  for (int r = 0; r < reps; ++r) {
+    bool any_dead = false;
+    for (int j = 0; j < Sr; ++j) any_dead = any_dead || dead[size_t(r) * Sr + j];
+    const uint64_t* C = base.data();
+    const int32_t* pr = nullptr;
+    if (any_dead) {
+      cost = base;
+      for (int i = 0; i < Dr; ++i)
+        for (int j = 0; j < Sr; ++j)
+          if (dead[size_t(r) * Sr + j]) cost[size_t(i) * Sr + j] = ETC_COST_INF;
+      solve_sketch(cost.data(), Dr, Sr, pair.data());
+      C = cost.data();
+      pr = pair.data();
+    } else {
+      if (base_pair.empty()) {
+        base_pair.resize(Dr);
+        solve_sketch(base.data(), Dr, Sr, base_pair.data());
+      }
+      pr = base_pair.data();
+    }
+    for (int i = 0; i < Dr; ++i)
+      if (pr[i] >= 0 && C[size_t(i) * Sr + pr[i]] < uint64_t(ETC_COST_INF)) P.home[r * Dr + i] = r * Sr + pr[i];
+  }
 }
 
 void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_parallel_cfg& dst) {

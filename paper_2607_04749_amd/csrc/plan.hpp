@@ -24,8 +24,10 @@ void validate(const etc_model_desc& m, const etc_parallel_cfg& src, const etc_pa
 void build_route_tensors(etc_plan_t& P);
 // routing context of a plan's host tables
 RouteCtx host_route_ctx(const etc_plan_t& P);
-// COST (D x S, bytes) on the host, for the migration sketch
-std::vector<uint64_t> host_cost_matrix(const etc_plan_t& P);
+// COST of one replica pair on the host (rows: a replica's target ranks)
+std::vector<uint64_t> host_replica_cost(const etc_plan_t& P);
+// the migration sketch, replica by replica, into P.home (dead: failed sources)
+void sketch_pairing(etc_plan_t& P, const std::vector<char>& dead);
 // layouts, routing, message layouts (host only); P.home must be set
 void build_host_plan(etc_plan_t& P);
 // virtual rank allocator (defrag.hip); returns an ETC_ status

@@ -77,6 +77,35 @@ def test_dp_sketch_stays_in_replicas(a, b):
         assert pair[d] // rs == d // rd
 
 
+DP_SKETCH_PAIRS = DP_PAIRS + [(P(2, 2, 4), P(1, 2, 2)), (P(1, 2, 2), P(2, 2, 4)),
+                               (P(2, 1, 3), P(1, 2, 3))]
+
+
+@pytest.mark.parametrize("a,b", DP_SKETCH_PAIRS)
+def test_dp_sketch_by_replica_equals_whole_matrix(a, b):
+    """The plan solves the sketch replica by replica; the oracle solves one
+    zero-padded assignment over the whole matrix, with infinite costs across
+    replicas and to failed ranks.  Their pairs of finite cost agree in number
+    and in total cost, with and without failed ranks (scale-in, scale-out and
+    equal DP)."""
+    m = MICRO_MODELS["gpt"]
+    fails = [None]
+    if a.dp > 1:
+        fails.append([1])
+        if a.tp * a.pp > 1:
+            fails.append([0, a.world - 1])
+    for failed in fails:
+        cost = oracle.matrices(m, a, b, failed=failed)["cost"]
+        opair, _ = oracle.sketch(cost)
+        ofin = [(d, int(p)) for d, p in enumerate(opair) if p >= 0 and cost[d, p] < oracle.COST_INF]
+        lp = etc.etc_plan(m, a, b, flags=HOST | etc.PLAN_SKETCH, failed=failed).pairing()
+        lfin = [(d, int(p)) for d, p in enumerate(lp) if p >= 0]
+        assert all(cost[d, p] < oracle.COST_INF for d, p in lfin), (a, b, failed)
+        assert len({p for _, p in lfin}) == len(lfin)
+        assert len(lfin) == len(ofin), (a, b, failed)
+        assert sum(int(cost[d, p]) for d, p in lfin) == sum(int(cost[d, p]) for d, p in ofin), (a, b, failed)
+
+
 @pytest.mark.parametrize("name", ["gpt", "llama_tied"])
 def test_dp_planner_matches_oracle(name):
     m = MICRO_MODELS[name]

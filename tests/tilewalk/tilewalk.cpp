@@ -184,10 +184,7 @@ int main(int argc, char** argv) {
     build_route_tensors(P);
     P.home.assign(D, -1);
     if (pairing == "sketch") {
-      auto c = host_cost_matrix(P);
-      solve_sketch(c.data(), D, S, P.home.data());
-      for (int d = 0; d < D; ++d)
-        if (P.home[d] >= 0 && c[size_t(d) * S + P.home[d]] >= ETC_COST_INF) P.home[d] = -1;
+      sketch_pairing(P, dead);
     } else if (pairing == "identity") {
       for (int d = 0; d < D && d < S; ++d)
         if (!dead[d] && P.src.replica(d) == P.dst.replica(d)) P.home[d] = d;
