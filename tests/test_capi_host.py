@@ -143,6 +143,37 @@ def test_rank_plan_send_layout_any_source():
         np.testing.assert_array_equal(p.send_layout(s)[0], oracle.send_layout(w.model, w.src, w.dst, s)[0])
 
 
+def _per_process_agree(m, a, b, failed=None):
+    whole = etc.etc_plan(m, a, b, flags=HOST | etc.PLAN_SKETCH, failed=failed)
+    pair = whole.pairing()
+    n = a.world + int((pair < 0).sum())
+    for q in range(n):
+        p = etc.etc_plan(m, a, b, rank=q, flags=HOST | etc.PLAN_SKETCH, failed=failed)
+        np.testing.assert_array_equal(p.pairing(), pair)
+        assert p.process(q) == whole.process(q)
+        for s in range(a.world):
+            for x, y in zip(p.send_layout(s), whole.send_layout(s)):
+                np.testing.assert_array_equal(x, y)
+        for d in range(b.world):
+            np.testing.assert_array_equal(p.recv_counts(d), whole.recv_counts(d))
+
+
+@pytest.mark.parametrize("wl", sorted(WORKLOADS))
+def test_per_process_plans_agree(wl):
+    """Each process derives the whole plan locally (Sec. III-B): the plans
+    built for every process agree on the sketch, the roles and every layout."""
+    w = WORKLOADS[wl]
+    _per_process_agree(w.model, w.src, w.dst)
+
+
+def test_per_process_plans_agree_random():
+    from randcfg import cases
+    for m, a, b in cases(24, base=0xA11):
+        _per_process_agree(m, a, b)
+        if a.dp > 1:
+            _per_process_agree(m, a, b, failed=[a.world - 1])
+
+
 @pytest.mark.parametrize("wl", sorted(WORKLOADS))
 def test_chunk_layout(wl):
     """Chunked migration (one state kind at a time): message s->d of kind k in
