@@ -318,6 +318,11 @@ enum { ETC_MAX_PEERS = 256 };
  * that kind, so its memory can be allocated per chunk and each source arena
  * released as soon as its kind has been packed.  Message s->d of kind k in a
  * chunk buffer is byte for byte section k of the full message s->d.
+ * Routing is per element, and the four arenas share one element layout, so
+ * in the one-kind calls `kind` only selects the element size: 2 bytes for
+ * ETC_KIND_PARAM_BF16, 4 for the other kinds.  Any further per-element
+ * state in that layout (the paper's "other states", e.g. an fp32 gradient)
+ * migrates through the same calls, passed as a kind of its element size.
  * etc_plan_chunk_layout: counts[d] = bytes of message s->d for this kind
  * (padded, 0 if nothing is routed), displs[d] = its byte offset in the chunk
  * buffer (multiple of 256), *total = chunk buffer length.  D entries each;
