@@ -179,8 +179,10 @@ typedef struct {
  * assignment problem, drop pairs in the padding.  Output pair[i] (M entries,
  * host) = the column paired with row i, or -1; *total (may be NULL) = the
  * kept pairs' summed cost.  Several optimal pairings may exist; any one is
- * returned.  Entries must be below 2^52.  Host only, O(k^3).
- * Errors: INVALID_ARG, UNSUPPORTED, NOMEM. */
+ * returned.  Host only, O(k^3), exact (integer arithmetic).
+ * Errors: INVALID_ARG (NULL, M or N outside 1..65536), UNSUPPORTED (an entry
+ * above 2^52, or min(M, N) times the largest entry above 2^64 - 1, the most a
+ * pairing's total could reach), NOMEM. */
 ETC_API int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* total);
 
 /* Options of etc_plan (NULL = all defaults: identity pairing, no failures,
@@ -288,7 +290,8 @@ ETC_API int etc_plan_recv_counts(const etc_plan_t* plan, int dst_rank, uint64_t*
  * device memory d_out, with one GPU kernel over every (source, target) pair
  * and every logical tensor (Sec. III-B, cost matrix; Sec. III-C, LCM items).
  * d_out must be 8-byte aligned.
- * Errors: INVALID_ARG (bad `which`, NULL, host-only plan), ALIGN, HIP. */
+ * Errors: INVALID_ARG (bad `which`, NULL, host-only plan), ALIGN,
+ * UNSUPPORTED (S * D above 2^31 - 1), HIP. */
 ETC_API int etc_cost_matrix(const etc_plan_t* plan, int which, uint64_t* d_out, void* stream);
 
 /* Pack: copy source rank src_rank's shards (src_arena[k] = its arena of kind

@@ -185,8 +185,12 @@ extern "C" {
 int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* total) {
   if (!cost || !pair) return fail(ETC_ERR_INVALID_ARG, "cost and pair must not be NULL");
   if (M < 1 || N < 1 || M > 65536 || N > 65536) return fail(ETC_ERR_INVALID_ARG, "bad matrix shape");
-  for (size_t i = 0; i < size_t(M) * N; ++i)
-    if (cost[i] > (uint64_t(1) << 52)) return fail(ETC_ERR_UNSUPPORTED, "cost entries must be below 2^52");
+  uint64_t top = 0;
+  for (size_t i = 0; i < size_t(M) * N; ++i) top = std::max(top, cost[i]);
+  if (top > (uint64_t(1) << 52)) return fail(ETC_ERR_UNSUPPORTED, "cost entries must not exceed 2^52");
+  // at most min(M, N) pairs: their total must fit the 64-bit result
+  if (top > 0 && uint64_t(std::min(M, N)) > UINT64_MAX / top)
+    return fail(ETC_ERR_UNSUPPORTED, "the total cost of a pairing could exceed 2^64 - 1");
   try {
     const uint64_t t = etc::solve_sketch(cost, M, N, pair);
     if (total) *total = t;
@@ -394,6 +398,9 @@ int etc_cost_matrix(const etc_plan_t* P, int which, uint64_t* d_out, void* strea
   if (which < ETC_CM_ROUTE || which > ETC_CM_COST) return fail(ETC_ERR_INVALID_ARG, "bad matrix selector");
   if (!d_out) return fail(ETC_ERR_INVALID_ARG, "d_out is NULL");
   if (!aligned(d_out, 8)) return fail(ETC_ERR_ALIGN, "d_out is not 8-byte aligned");
+  // one matrix cell per (source, target) pair, indexed in 32 bits by the kernel
+  if (uint64_t(P->src.world()) * uint64_t(P->dst.world()) > uint64_t(INT32_MAX))
+    return fail(ETC_ERR_UNSUPPORTED, "a cost matrix is limited to 2^31 - 1 cells");
   const etc::RouteCtx ctx{P->src.tp, P->src.pp, P->src.dp, P->dst.tp, P->dst.pp, P->dst.dp,
                          P->d_failed};
   hipError_t e = etc::launch_cost(P->d_route_tensors, int(P->route_tensors.size()), P->d_home, ctx,

@@ -5,10 +5,11 @@
 // solved, and pairs involving padding are dropped.  The square problem is
 // solved with the Kuhn-Munkres (Hungarian) method in its shortest-augmenting-
 // path form with row and column potentials: O(k^3), microseconds for the
-// k <= 128 of a PP x TP grid.
+// k <= 128 of a PP x TP grid.  The potentials drift while rows are added (on
+// some matrices to k times the largest entry), so they are 128-bit: entries
+// below 2^53 and k <= 65536 keep them under 2^70.
 #include <algorithm>
 #include <cstdint>
-#include <limits>
 #include <vector>
 
 #include "plan.hpp"
@@ -17,11 +18,12 @@ namespace etc {
 
 uint64_t solve_sketch(const uint64_t* cost, int M, int N, int32_t* pair) {
   const int k = std::max(M, N);
-  auto c = [&](int i, int j) -> int64_t {  // 1-based rows / columns, zero padding
-    return (i <= M && j <= N) ? int64_t(cost[size_t(i - 1) * N + (j - 1)]) : 0;
+  using Pot = __int128;
+  auto c = [&](int i, int j) -> Pot {  // 1-based rows / columns, zero padding
+    return (i <= M && j <= N) ? Pot(cost[size_t(i - 1) * N + (j - 1)]) : 0;
   };
-  const int64_t INF = std::numeric_limits<int64_t>::max() / 4;
-  std::vector<int64_t> u(k + 1, 0), v(k + 1, 0), slack(k + 1);
+  const Pot INF = Pot(1) << 100;
+  std::vector<Pot> u(k + 1, 0), v(k + 1, 0), slack(k + 1);
   std::vector<int> row_of(k + 1, 0), prev(k + 1, 0);  // row_of[j]: row matched to column j
   std::vector<char> visited(k + 1);
   for (int i = 1; i <= k; ++i) {
@@ -33,11 +35,11 @@ uint64_t solve_sketch(const uint64_t* cost, int M, int N, int32_t* pair) {
     do {
       visited[j0] = 1;
       const int i0 = row_of[j0];
-      int64_t delta = INF;
+      Pot delta = INF;
       int j1 = 0;
       for (int j = 1; j <= k; ++j) {
         if (visited[j]) continue;
-        const int64_t reduced = c(i0, j) - u[i0] - v[j];
+        const Pot reduced = c(i0, j) - u[i0] - v[j];
         if (reduced < slack[j]) {
           slack[j] = reduced;
           prev[j] = j0;

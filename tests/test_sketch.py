@@ -254,3 +254,32 @@ def test_direct_refer_micro_matches_oracle():
                 np.testing.assert_array_equal(dsp, odsp)
                 assert tot == otot
             p.free()
+
+
+@pytest.mark.parametrize("k", [64, 2048])
+def test_sketch_closed_form_with_drifting_potentials(k):
+    """c_ij = 2^52 - 977 i j: by the rearrangement inequality the identity is
+    the unique optimum, with total k 2^52 - 977 sum(i^2).  On this matrix the
+    solver's dual potentials drift to k times the largest entry (2^63 at
+    k = 2048, past a signed 64-bit range), so it checks their width."""
+    C = 1 << 52
+    i = np.arange(k, dtype=np.uint64)
+    M = np.uint64(C) - np.outer(i, i) * np.uint64(977)
+    pair, total = etc.etc_sketch(M)
+    np.testing.assert_array_equal(pair, np.arange(k))
+    assert total == k * C - 977 * sum(x * x for x in range(k))
+
+
+def test_sketch_total_range():
+    """The summed cost of a pairing must fit 64 bits: min(M, N) times the
+    largest entry may not exceed 2^64 - 1; entries may not exceed 2^52."""
+    pair, total = etc.etc_sketch(np.full((2, 3), 1 << 52, np.uint64))
+    assert total == 2 << 52
+    big = np.zeros((4097, 4097), np.uint64)
+    big[0, 0] = 1 << 52
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_sketch(big)
+    assert e.value.code == etc.ERR_UNSUPPORTED
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_sketch(np.full((2, 2), (1 << 52) + 1, np.uint64))
+    assert e.value.code == etc.ERR_UNSUPPORTED
