@@ -161,8 +161,8 @@ def main():
     ap.add_argument("--mode", choices=("direct", "chunked", "coalesced", "refer"), default="direct")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU's share of the migration; runs on more than one GPU "
-              "are not part of this build (--gpus must be 1)", file=sys.stderr)
+        print("bench.py measures one GPU's share of the migration; multi-GPU runs are not "
+              "supported (--gpus must be 1)", file=sys.stderr)
         sys.exit(2)
     if args.identity and args.mode == "coalesced":
         print("--identity and --mode coalesced exclude each other", file=sys.stderr)
