@@ -154,3 +154,40 @@ def test_error_paths_on_device():
         etc.etc_cost_matrix(plan, etc.CM_ROUTE, out.data_ptr() + 4)
     assert e.value.code == etc.ERR_ALIGN
     torch.cuda.synchronize()
+
+
+def test_empty_launches():
+    """Identity configuration with direct Refer: every message is empty, so
+    each pack and unpack (all kinds, or one) has nothing to copy.  They return
+    at once, even with NULL buffers, and leave the target untouched; Refer then
+    copies every byte.  Without the flag, Refer is the empty call."""
+    w = WORKLOADS["tiny-gpt"]
+    a = w.src
+    plan = etc.etc_plan(w.model, a, a, flags=etc.PLAN_DIRECT_REFER)
+    src = seeded_arenas(w.model, a, range(a.world), w.seed)
+    say("tiny-gpt identity with direct Refer: empty packs and unpacks")
+    for s in range(a.world):
+        assert plan.send_layout(s)[3] == 0
+        etc.etc_pack(plan, s, src[s], None)
+        for k in range(4):
+            etc.etc_pack_kind(plan, s, k, src[s][k], None)
+    for d in range(a.world):
+        assert int(plan.recv_counts(d).sum()) == 0
+        dst = alloc(plan.arena_elems(etc.SIDE_DST, d))
+        for x in dst:
+            x.fill_(0x5A)
+        etc.etc_unpack(plan, d, [None] * plan.S, dst)
+        for k in range(4):
+            etc.etc_unpack_kind(plan, d, k, [None] * plan.S, dst[k])
+        torch.cuda.synchronize()
+        assert all(bool((x == 0x5A).all()) for x in dst)
+        etc.etc_refer(plan, d, src[d], dst)
+        torch.cuda.synchronize()
+        for k in range(4):
+            assert equal(dst[k], src[d][k]), f"target {d} kind {k}"
+    plain = etc.etc_plan(w.model, a, a)
+    assert plain.refer_bytes(0) == 0
+    dst = alloc(plain.arena_elems(etc.SIDE_DST, 0))
+    etc.etc_refer(plain, 0, src[0], dst)
+    torch.cuda.synchronize()
+    assert all(bool((x == 0).all()) for x in dst)
