@@ -14,7 +14,7 @@
 // A tile's descriptor is uniform across the workgroup (scalar loads).
 // Within a tile, each thread moves 16-byte vectors in batches: 16 loads in
 // flight, then the 16 stores, for contiguous rows (a workgroup streams 64 KB
-// per batch); 4 for strided rows.  Loads and stores are non-temporal since
+// per batch); 8, predicated, for strided rows.  Loads and stores are non-temporal since
 // nothing is reused.  On MI355X this shape measured best of the ones tried
 // (deeper batches at low occupancy beat more resident waves with shallow
 // batches: the memory system is saturated and fewer, larger contiguous
@@ -43,7 +43,7 @@ struct CopyArgs {
 };
 
 constexpr int kRowBatch = 16;  // vectors in flight per thread, contiguous rows
-constexpr int kBatch2D = 4;    // vectors in flight per thread, strided rows
+constexpr int kBatch2D = 8;    // vectors in flight per thread, strided rows (predicated)
 
 // Copy nr rows of row_bytes bytes (16-byte aligned starts, row_bytes a
 // multiple of 16 when nr > 1) from src (row pitch sld bytes) to dst (pitch dld).
@@ -86,7 +86,10 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
           reinterpret_cast<u32x4*>(dst + uint64_t(i) * 16));
     return;
   }
-  for (; i + (kBatch2D - 1) * kCopyThreads < nv; i += kBatch2D * kCopyThreads) {
+  // Strided rows: a tile holds a few thousand vectors, not a multiple of the
+  // batch, so the last batch is predicated rather than finished one vector at
+  // a time.
+  for (; i < nv; i += kBatch2D * kCopyThreads) {
     u32x4 v[kBatch2D];
     uint32_t r[kBatch2D], c[kBatch2D];
 #pragma unroll
@@ -94,19 +97,15 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
       const uint32_t idx = i + u * kCopyThreads;
       r[u] = idx / vpr;
       c[u] = idx - r[u] * vpr;
-      v[u] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4*>(src + r[u] * sld + uint64_t(c[u]) * 16));
+      if (idx < nv)
+        v[u] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(src + r[u] * sld + uint64_t(c[u]) * 16));
     }
 #pragma unroll
     for (int u = 0; u < kBatch2D; ++u)
-      __builtin_nontemporal_store(v[u],
-                                  reinterpret_cast<u32x4*>(dst + r[u] * dld + uint64_t(c[u]) * 16));
-  }
-  for (; i < nv; i += kCopyThreads) {
-    const uint32_t r = i / vpr, c = i - r * vpr;
-    __builtin_nontemporal_store(
-        __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + r * sld + uint64_t(c) * 16)),
-        reinterpret_cast<u32x4*>(dst + r * dld + uint64_t(c) * 16));
+      if (i + u * kCopyThreads < nv)
+        __builtin_nontemporal_store(
+            v[u], reinterpret_cast<u32x4*>(dst + r[u] * dld + uint64_t(c[u]) * 16));
   }
 }
 
