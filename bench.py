@@ -147,7 +147,25 @@ def cpu_baseline(w, pairing, layers=4, direct_refer=False):
     return {"value": round(alg / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"tensors of layers {held[0]}-{held[-1]} ({len(sample)} tensors): pack of source {s0} + "
                       f"unpack of target {d0}, {pairing} pairing, {alg / 1e9:.3f} GB algorithmic, "
-                      f"{dt:.2f} s"}
+                      f"{dt:.2f} s on one thread of {host_cpu()}"}
+
+
+def host_cpu():
+    """Model name of the host CPU and the logical CPUs this process may use."""
+    name = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count()
+    return f"{name} ({n} logical CPUs available)"
 
 
 def main():
