@@ -334,7 +334,7 @@ int etc_plan_arena_elems(const etc_plan_t* P, int side, int rank, uint64_t* elem
   int rc = check_side_rank(P, side, rank);
   if (rc) return rc;
   if (!elems) return fail(ETC_ERR_INVALID_ARG, "elems is NULL");
-  *elems = (side == ETC_SIDE_SRC ? P->src_layout : P->dst_layout)[rank].elems;
+  *elems = (side == ETC_SIDE_SRC ? P->src_lay(rank) : P->dst_lay(rank)).elems;
   return ETC_OK;
 }
 
@@ -342,14 +342,14 @@ int etc_plan_num_pieces(const etc_plan_t* P, int side, int rank, int* n) {
   int rc = check_side_rank(P, side, rank);
   if (rc) return rc;
   if (!n) return fail(ETC_ERR_INVALID_ARG, "n is NULL");
-  *n = int((side == ETC_SIDE_SRC ? P->src_layout : P->dst_layout)[rank].pieces.size());
+  *n = int((side == ETC_SIDE_SRC ? P->src_lay(rank) : P->dst_lay(rank)).pieces.size());
   return ETC_OK;
 }
 
 int etc_plan_piece(const etc_plan_t* P, int side, int rank, int index, etc_piece_info* out) {
   int rc = check_side_rank(P, side, rank);
   if (rc) return rc;
-  const auto& L = (side == ETC_SIDE_SRC ? P->src_layout : P->dst_layout)[rank];
+  const auto& L = side == ETC_SIDE_SRC ? P->src_lay(rank) : P->dst_lay(rank);
   if (!out || index < 0 || index >= int(L.pieces.size()))
     return fail(ETC_ERR_INVALID_ARG, "bad piece index");
   const etc::Piece& p = L.pieces[index];
@@ -373,11 +373,16 @@ int etc_plan_send_layout(const etc_plan_t* P, int s, uint64_t* counts, uint64_t*
   int rc = check_side_rank(P, ETC_SIDE_SRC, s);
   if (rc) return rc;
   const int D = P->dst.world();
+  // an empty message is reported where the next one would start
+  uint32_t k = P->src_first[s];
+  uint64_t cur = 0;
   for (int d = 0; d < D; ++d) {
-    const size_t sd = size_t(s) * D + d;
-    if (counts) counts[d] = P->msg_elems[sd] * 14;
-    if (msg_bytes) msg_bytes[d] = P->msg_npad[sd] * 14;
-    if (displs) displs[d] = P->msg_displ[sd];
+    const bool has = k < P->src_first[s + 1] && P->msgs[k].d == d;
+    const etc_plan_s::Message* m = has ? &P->msgs[k++] : nullptr;
+    if (counts) counts[d] = m ? m->elems * 14 : 0;
+    if (msg_bytes) msg_bytes[d] = m ? m->npad * 14 : 0;
+    if (displs) displs[d] = m ? m->displ : (cur + 255) / 256 * 256;
+    if (m) cur = m->displ + m->npad * 14;
   }
   if (total) *total = P->sendbuf_bytes[s];
   return ETC_OK;
@@ -387,8 +392,12 @@ int etc_plan_recv_counts(const etc_plan_t* P, int d, uint64_t* counts) {
   int rc = check_side_rank(P, ETC_SIDE_DST, d);
   if (rc) return rc;
   if (!counts) return fail(ETC_ERR_INVALID_ARG, "counts is NULL");
-  const int S = P->src.world(), D = P->dst.world();
-  for (int s = 0; s < S; ++s) counts[s] = P->msg_elems[size_t(s) * D + d] * 14;
+  const int S = P->src.world();
+  for (int s = 0; s < S; ++s) counts[s] = 0;
+  for (uint32_t k = P->dst_first[d]; k < P->dst_first[d + 1]; ++k) {
+    const etc_plan_s::Message& m = P->msgs[P->dst_msgs[k]];
+    counts[m.s] = m.elems * 14;
+  }
   return ETC_OK;
 }
 
@@ -421,10 +430,9 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
   if (!aligned(send_buf, 256)) return fail(ETC_ERR_ALIGN, "send_buf is not 256-byte aligned");
   void* arenas[4];
   for (int k = 0; k < 4; ++k) arenas[k] = const_cast<void*>(src_arena[k]);
-  const int D = P->dst.world();
   void* peers[ETC_MAX_PEERS];
-  for (size_t i = 0; i < t.peers.size(); ++i)
-    peers[i] = static_cast<char*>(send_buf) + P->msg_displ[size_t(s) * D + t.peers[i]];
+  for (size_t i = 0; i < t.peers.size(); ++i)  // the pack's peers are s's messages, in order
+    peers[i] = static_cast<char*>(send_buf) + P->msgs[P->src_first[s] + i].displ;
   hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
                                   P->copy_lds_reserve, 0xFu, etc::kMsgSections, arenas, peers,
                                   int(t.peers.size()), static_cast<hipStream_t>(stream));
@@ -463,10 +471,14 @@ int etc_plan_chunk_layout(const etc_plan_t* P, int s, int kind, uint64_t* counts
   const int i = kind == ETC_KIND_PARAM_BF16 ? 0 : 1;
   const uint64_t es = i == 0 ? 2 : 4;
   const int D = P->dst.world();
+  uint32_t k = P->src_first[s];
+  uint64_t cur = 0;
   for (int d = 0; d < D; ++d) {
-    const size_t sd = size_t(s) * D + d;
-    if (counts) counts[d] = P->msg_npad[sd] * es;
-    if (displs) displs[d] = P->chunk_displ[i][sd];
+    const bool has = k < P->src_first[s + 1] && P->msgs[k].d == d;
+    const etc_plan_s::Message* m = has ? &P->msgs[k++] : nullptr;
+    if (counts) counts[d] = m ? m->npad * es : 0;
+    if (displs) displs[d] = m ? m->chunk_displ[i] : (cur + 255) / 256 * 256;
+    if (m) cur = m->chunk_displ[i] + m->npad * es;
   }
   if (total) *total = P->chunk_bytes[i][s];
   return ETC_OK;
@@ -486,11 +498,10 @@ int etc_pack_kind(const etc_plan_t* P, int s, int kind, const void* src_arena, v
     return fail(ETC_ERR_ALIGN, "src_arena and chunk_buf must be 256-byte aligned");
   void* arenas[4] = {nullptr, nullptr, nullptr, nullptr};
   arenas[kind] = const_cast<void*>(src_arena);
-  const int D = P->dst.world();
   const int i = kind == ETC_KIND_PARAM_BF16 ? 0 : 1;
   void* peers[ETC_MAX_PEERS];
   for (size_t j = 0; j < t.peers.size(); ++j)
-    peers[j] = static_cast<char*>(chunk_buf) + P->chunk_displ[i][size_t(s) * D + t.peers[j]];
+    peers[j] = static_cast<char*>(chunk_buf) + P->msgs[P->src_first[s] + j].chunk_displ[i];
   hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
                                   P->copy_lds_reserve, 1u << kind, etc::kMsgOneKind, arenas, peers,
                                   int(t.peers.size()), static_cast<hipStream_t>(stream));

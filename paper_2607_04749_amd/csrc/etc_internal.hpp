@@ -135,30 +135,52 @@ struct etc_plan_s {
   uint32_t flags = 0;
   std::vector<etc::LogicalTensor> tensors;
   std::vector<etc::RouteTensor> route_tensors;
+  // layouts of the ranks of one data-parallel replica: every replica has the
+  // same (rank r's layout is that of r mod replica size)
   std::vector<etc::RankLayout> src_layout, dst_layout;
+  const etc::RankLayout& src_lay(int s) const { return src_layout[size_t(s % src.replica_size())]; }
+  const etc::RankLayout& dst_lay(int d) const { return dst_layout[size_t(d % dst.replica_size())]; }
   std::vector<int32_t> home;  // [d]: source rank paired with target d (migration sketch), or -1
   std::vector<uint32_t> failed_bits;  // bitmap of source ranks whose states are lost
 
-  // messages, indexed [s * D + d]
   struct MsgBox {
     int32_t tensor, role_d;
     int64_t r0, r1, c0, c1;
     uint64_t moff;
   };
-  std::vector<std::vector<MsgBox>> msg;
+  // One non-empty message s -> d: its boxes in d's arena order.
+  struct Message {
+    int32_t s = 0, d = 0;
+    std::vector<MsgBox> boxes;
+    uint64_t elems = 0;  // routed elements
+    uint64_t npad = 0;   // padded elements per kind section
+    uint64_t displ = 0;  // byte offset in s's send buffer
+    // byte offset in s's chunk buffer of a 2-byte (index 0) or 4-byte (1) kind
+    uint64_t chunk_displ[2] = {0, 0};
+  };
+  // Every non-empty message, ordered by source, then target.  Only these are
+  // stored (a target hears from a few sources), so a plan's host tables grow
+  // with the number of ranks, not with its square.
+  std::vector<Message> msgs;
+  std::vector<uint32_t> src_first;  // [S + 1]: msgs[src_first[s] .. src_first[s + 1]) are s's
+  std::vector<uint32_t> dst_msgs;   // indices into msgs, by target, then source
+  std::vector<uint32_t> dst_first;  // [D + 1]: dst_msgs[dst_first[d] .. dst_first[d + 1]) are d's
+  // the message s -> d, or nullptr when nothing is routed from s to d
+  const Message* find_msg(int s, int d) const {
+    size_t lo = src_first[size_t(s)], hi = src_first[size_t(s) + 1];
+    while (lo < hi) {
+      const size_t mid = (lo + hi) / 2;
+      if (msgs[mid].d < d) lo = mid + 1;
+      else hi = mid;
+    }
+    return lo < src_first[size_t(s) + 1] && msgs[lo].d == d ? &msgs[lo] : nullptr;
+  }
   // [d]: boxes that d's paired source keeps (Refer), copied arena to arena by
   // etc_refer when the plan has ETC_PLAN_DIRECT_REFER; no message carries them
   std::vector<std::vector<MsgBox>> refer;
   std::vector<uint64_t> refer_elems;
-  std::vector<uint64_t> msg_elems;  // routed elements
-  std::vector<uint64_t> msg_npad;   // padded elements per kind section
-  std::vector<uint64_t> msg_displ;  // byte displacement in the sender's buffer
-  std::vector<uint64_t> sendbuf_bytes;
-  // chunked migration, one state kind at a time: message s->d of a 2-byte
-  // (index 0) or 4-byte (index 1) kind at chunk_displ[i][s * D + d] in a
-  // chunk buffer of chunk_bytes[i][s] bytes
-  std::vector<uint64_t> chunk_displ[2];
-  std::vector<uint64_t> chunk_bytes[2];
+  std::vector<uint64_t> sendbuf_bytes;   // [S]: send buffer length
+  std::vector<uint64_t> chunk_bytes[2];  // [S]: chunk buffer length of a 2-byte / 4-byte kind
 
   // device side
   int device = -1;

@@ -217,25 +217,26 @@ void build_host_plan(etc_plan_t& P) {
   const int nt = int(P.tensors.size());
   const int S = P.src.world(), D = P.dst.world();
   if (int(P.home.size()) != D) fail(ETC_ERR_INVALID_ARG, "internal: pairing not set");
-  P.src_layout.resize(S);
-  P.dst_layout.resize(D);
-  for (int s = 0; s < S; ++s) P.src_layout[s] = build_layout(P.tensors, P.src, m.num_layers, s);
-  for (int d = 0; d < D; ++d) P.dst_layout[d] = build_layout(P.tensors, P.dst, m.num_layers, d);
+  const int Sr = P.src.replica_size(), Dr = P.dst.replica_size();
+  P.src_layout.resize(Sr);
+  P.dst_layout.resize(Dr);
+  for (int s = 0; s < Sr; ++s) P.src_layout[s] = build_layout(P.tensors, P.src, m.num_layers, s);
+  for (int d = 0; d < Dr; ++d) P.dst_layout[d] = build_layout(P.tensors, P.dst, m.num_layers, d);
 
   if (P.route_tensors.size() != size_t(nt)) build_route_tensors(P);
 
   const RouteCtx ctx = host_route_ctx(P);
   // Route every target piece: per target rank, per piece in arena order, the
   // sources that send part of it.  Messages list boxes in that order.
-  P.msg.assign(size_t(S) * D, {});
-  P.msg_elems.assign(size_t(S) * D, 0);
-  P.msg_npad.assign(size_t(S) * D, 0);
+  P.msgs.clear();
   P.refer.assign(D, {});
   P.refer_elems.assign(D, 0);
   const bool direct_refer = (P.flags & ETC_PLAN_DIRECT_REFER) != 0;
   std::vector<int> cand;
+  std::vector<etc_plan_s::Message> to_d;  // messages to the current target, by first box
   for (int d = 0; d < D; ++d) {
-    for (const Piece& q : P.dst_layout[d].pieces) {
+    to_d.clear();
+    for (const Piece& q : P.dst_lay(d).pieces) {
       const RouteTensor& rt = P.route_tensors[q.tensor];
       uint64_t got = 0;
       candidate_senders(rt, d, P.home[d], ctx, &cand);
@@ -263,57 +264,66 @@ void build_host_plan(etc_plan_t& P) {
           P.refer_elems[d] += n;
           continue;
         }
-        const size_t sd = size_t(s) * D + d;
-        b.moff = P.msg_npad[sd];
-        P.msg_npad[sd] += uint64_t(round_up(int64_t(n), 8));
-        P.msg_elems[sd] += n;
-        P.msg[sd].push_back(b);
+        auto it = std::find_if(to_d.begin(), to_d.end(), [&](const etc_plan_s::Message& x) { return x.s == s; });
+        if (it == to_d.end()) {
+          to_d.emplace_back();
+          it = to_d.end() - 1;
+          it->s = s;
+          it->d = d;
+        }
+        b.moff = it->npad;
+        it->npad += uint64_t(round_up(int64_t(n), 8));
+        it->elems += n;
+        it->boxes.push_back(b);
       }
       if (got != q.elems())
         fail(ETC_ERR_UNRECOVERABLE, "no live source rank holds part of " + P.tensors[q.tensor].name +
                                         " needed by target rank " + std::to_string(d));
     }
+    for (auto& x : to_d) P.msgs.push_back(std::move(x));
   }
+  std::sort(P.msgs.begin(), P.msgs.end(), [](const etc_plan_s::Message& a, const etc_plan_s::Message& b) {
+    return a.s != b.s ? a.s < b.s : a.d < b.d;
+  });
+  if (P.msgs.size() > size_t(UINT32_MAX)) fail(ETC_ERR_UNSUPPORTED, "too many messages");
+  P.src_first.assign(size_t(S) + 1, 0);
+  P.dst_first.assign(size_t(D) + 1, 0);
+  for (const auto& x : P.msgs) {
+    ++P.src_first[size_t(x.s) + 1];
+    ++P.dst_first[size_t(x.d) + 1];
+  }
+  for (int s = 0; s < S; ++s) P.src_first[s + 1] += P.src_first[s];
+  for (int d = 0; d < D; ++d) P.dst_first[d + 1] += P.dst_first[d];
   // a copy launch addresses its peers' messages through a fixed table
-  std::vector<int> senders(D, 0);
-  for (int s = 0; s < S; ++s) {
-    int receivers = 0;
-    for (int d = 0; d < D; ++d)
-      if (!P.msg[size_t(s) * D + d].empty()) {
-        ++receivers;
-        ++senders[d];
-      }
-    if (receivers > ETC_MAX_PEERS)
+  for (int s = 0; s < S; ++s)
+    if (P.src_first[s + 1] - P.src_first[s] > uint32_t(ETC_MAX_PEERS))
       fail(ETC_ERR_UNSUPPORTED, "source rank " + std::to_string(s) + " feeds more than ETC_MAX_PEERS targets");
-  }
   for (int d = 0; d < D; ++d)
-    if (senders[d] > ETC_MAX_PEERS)
+    if (P.dst_first[d + 1] - P.dst_first[d] > uint32_t(ETC_MAX_PEERS))
       fail(ETC_ERR_UNSUPPORTED, "more than ETC_MAX_PEERS sources feed target rank " + std::to_string(d));
-  P.msg_displ.assign(size_t(S) * D, 0);
+  {  // per target, by source: the messages are sorted by source, so a stable fill keeps that order
+    std::vector<uint32_t> fill(P.dst_first.begin(), P.dst_first.end() - 1);
+    P.dst_msgs.assign(P.msgs.size(), 0);
+    for (uint32_t k = 0; k < uint32_t(P.msgs.size()); ++k) P.dst_msgs[fill[size_t(P.msgs[k].d)]++] = k;
+  }
+  // Send buffers: messages in target order, each at a multiple of 256 bytes;
+  // chunk buffers the same, one kind section each.  An empty message takes no
+  // room, so its (reported) offset is where the next one would start.
   P.sendbuf_bytes.assign(S, 0);
+  for (int i = 0; i < 2; ++i) P.chunk_bytes[i].assign(S, 0);
   for (int s = 0; s < S; ++s) {
-    uint64_t cur = 0;
-    for (int d = 0; d < D; ++d) {
-      cur = uint64_t(round_up(int64_t(cur), 256));
-      P.msg_displ[size_t(s) * D + d] = cur;
-      cur += P.msg_npad[size_t(s) * D + d] * 14;
+    uint64_t cur = 0, cur_k[2] = {0, 0};
+    for (uint32_t k = P.src_first[s]; k < P.src_first[s + 1]; ++k) {
+      etc_plan_s::Message& x = P.msgs[k];
+      x.displ = uint64_t(round_up(int64_t(cur), 256));
+      cur = x.displ + x.npad * 14;
+      for (int i = 0; i < 2; ++i) {
+        x.chunk_displ[i] = uint64_t(round_up(int64_t(cur_k[i]), 256));
+        cur_k[i] = x.chunk_displ[i] + x.npad * (i == 0 ? 2 : 4);
+      }
     }
     P.sendbuf_bytes[s] = uint64_t(round_up(int64_t(cur), 256));
-  }
-  // chunk layouts: the same messages, one kind section each
-  for (int i = 0; i < 2; ++i) {
-    const uint64_t es = i == 0 ? 2 : 4;
-    P.chunk_displ[i].assign(size_t(S) * D, 0);
-    P.chunk_bytes[i].assign(S, 0);
-    for (int s = 0; s < S; ++s) {
-      uint64_t cur = 0;
-      for (int d = 0; d < D; ++d) {
-        cur = uint64_t(round_up(int64_t(cur), 256));
-        P.chunk_displ[i][size_t(s) * D + d] = cur;
-        cur += P.msg_npad[size_t(s) * D + d] * es;
-      }
-      P.chunk_bytes[i][s] = uint64_t(round_up(int64_t(cur), 256));
-    }
+    for (int i = 0; i < 2; ++i) P.chunk_bytes[i][s] = uint64_t(round_up(int64_t(cur_k[i]), 256));
   }
 }
 

@@ -98,23 +98,21 @@ void add_box(std::vector<CopyBox>& v, uint32_t& tiles, uint64_t a_off, int64_t a
 
 std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<int32_t>* peers,
                                       uint64_t* bytes) {
-  const int D = P.dst.world();
   std::vector<CopyBox> v;
   uint32_t tiles = 0;
   uint64_t moved = 0;
-  const RankLayout& L = P.src_layout[s];
+  const RankLayout& L = P.src_lay(s);
   peers->clear();
-  for (int d = 0; d < D; ++d) {
-    const size_t sd = size_t(s) * D + d;
-    if (P.msg[sd].empty()) continue;
+  for (uint32_t k = P.src_first[s]; k < P.src_first[s + 1]; ++k) {  // targets ascending
+    const etc_plan_s::Message& m = P.msgs[k];
     const int slot = int(peers->size());
     if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "one source feeds more than ETC_MAX_PEERS targets");
-    peers->push_back(d);
-    for (const auto& b : P.msg[sd]) {
+    peers->push_back(m.d);
+    for (const auto& b : m.boxes) {
       const int role_s = role_on(P.route_tensors[b.tensor].src_stage, P.src.pp_of(s));
       const Piece& p = L.pieces[L.piece_of_tensor[role_s][b.tensor]];
       const uint64_t a_off = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
-      add_box(v, tiles, a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot, true,
+      add_box(v, tiles, a_off, p.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, m.npad, slot, true,
               b.c1 - b.c0);
       moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
     }
@@ -128,22 +126,20 @@ std::vector<CopyBox> build_pack_boxes(const etc_plan_t& P, int s, std::vector<in
 
 std::vector<CopyBox> build_unpack_boxes(const etc_plan_t& P, int d, std::vector<int32_t>* peers,
                                         uint64_t* bytes) {
-  const int S = P.src.world(), D = P.dst.world();
   std::vector<CopyBox> v;
   uint32_t tiles = 0;
   uint64_t moved = 0;
-  const RankLayout& L = P.dst_layout[d];
+  const RankLayout& L = P.dst_lay(d);
   peers->clear();
-  for (int s = 0; s < S; ++s) {
-    const size_t sd = size_t(s) * D + d;
-    if (P.msg[sd].empty()) continue;
+  for (uint32_t k = P.dst_first[d]; k < P.dst_first[d + 1]; ++k) {  // sources ascending
+    const etc_plan_s::Message& m = P.msgs[P.dst_msgs[k]];
     const int slot = int(peers->size());
     if (slot >= ETC_MAX_PEERS) fail(ETC_ERR_UNSUPPORTED, "more than ETC_MAX_PEERS sources feed one target");
-    peers->push_back(s);
-    for (const auto& b : P.msg[sd]) {
+    peers->push_back(m.s);
+    for (const auto& b : m.boxes) {
       const Piece& q = L.pieces[L.piece_of_tensor[b.role_d][b.tensor]];
       const uint64_t a_off = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
-      add_box(v, tiles, a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, P.msg_npad[sd], slot, false,
+      add_box(v, tiles, a_off, q.ld(), b.r1 - b.r0, b.c1 - b.c0, b.moff, m.npad, slot, false,
               b.c1 - b.c0);
       moved += uint64_t((b.r1 - b.r0) * (b.c1 - b.c0)) * 14;
     }
@@ -161,8 +157,8 @@ std::vector<CopyBox> build_refer_boxes(const etc_plan_t& P, int d, uint64_t* byt
   uint64_t moved = 0;
   const int h = P.home[d];
   if (h >= 0) {
-    const RankLayout& L = P.dst_layout[d];
-    const RankLayout& H = P.src_layout[h];
+    const RankLayout& L = P.dst_lay(d);
+    const RankLayout& H = P.src_lay(h);
     for (const auto& b : P.refer[d]) {
       const int role_s = role_on(P.route_tensors[b.tensor].src_stage, P.src.pp_of(h));
       const Piece& p = H.pieces[H.piece_of_tensor[role_s][b.tensor]];

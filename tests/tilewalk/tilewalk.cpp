@@ -39,6 +39,12 @@ static void merge_equal(std::vector<Iv> w, std::vector<Iv> want, const std::stri
     if (m[i].lo != mw[i].lo || m[i].hi != mw[i].hi) { FAIL("%s: coverage differs", what.c_str()); return; }
 }
 
+// padded elements per kind section of message s -> d (0 when empty)
+static uint64_t npad_of(const etc_plan_t& P, int s, int d) {
+  const auto* m = P.find_msg(s, d);
+  return m ? m->npad : 0;
+}
+
 // Replay one launch exactly as the kernel walks it.  peer_bytes[p] = length of
 // peer p's message; W[k][p] collects message writes (pack), A[k] arena writes.
 static void replay(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask, uint32_t G,
@@ -96,15 +102,15 @@ static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
         const uint32_t mask = sectioned ? 0xFu : (1u << k);
         if (sectioned && k) break;
         std::vector<uint64_t> pb;
-        for (int d : peers) pb.push_back(P.msg_npad[size_t(s) * D + d] * (sectioned ? 14 : (k ? 4 : 2)));
+        for (int d : peers) pb.push_back(npad_of(P, s, d) * (sectioned ? 14 : (k ? 4 : 2)));
         std::vector<std::vector<Iv>> W[4]; std::vector<Iv> A[4];
         for (int kk = 0; kk < 4; ++kk) W[kk].assign(peers.size(), {});
-        replay(v, true, sectioned, mask, grid, P.src_layout[s].elems, pb, W, A);
+        replay(v, true, sectioned, mask, grid, P.src_lay(s).elems, pb, W, A);
         for (int kk = 0; kk < 4; ++kk) {
           if (!(mask & (1u << kk))) continue;
           const int es = kk ? 4 : 2;
           for (size_t i = 0; i < peers.size(); ++i) {
-            const uint64_t npad = P.msg_npad[size_t(s) * D + peers[i]];
+            const uint64_t npad = npad_of(P, s, peers[i]);
             const uint64_t b0 = sectioned ? section_byte(npad, kk) : 0;
             merge_equal(W[kk][i], {{b0, b0 + npad * es}}, std::string(name) + " pack s" + std::to_string(s) + " peer " + std::to_string(i));
           }
@@ -118,26 +124,26 @@ static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
         const uint32_t mask = sectioned ? 0xFu : (1u << k);
         if (sectioned && k) break;
         std::vector<uint64_t> pb;
-        for (int s : peers) pb.push_back(P.msg_npad[size_t(s) * D + d] * (sectioned ? 14 : (k ? 4 : 2)));
+        for (int s : peers) pb.push_back(npad_of(P, s, d) * (sectioned ? 14 : (k ? 4 : 2)));
         std::vector<std::vector<Iv>> W[4]; std::vector<Iv> A[4];
-        replay(v, false, sectioned, mask, grid, P.dst_layout[d].elems, pb, W, A);
+        replay(v, false, sectioned, mask, grid, P.dst_lay(d).elems, pb, W, A);
         if (P.flags & ETC_PLAN_DIRECT_REFER) {  // Refer writes complete the target
           uint64_t rb = 0;
           auto rv = build_refer_boxes(P, d, &rb);
           const int h = P.home[d];
           if (h < 0 && rv.size() > 1) FAIL("refer boxes without a paired source");
           if (h >= 0) {
-            const uint64_t se = P.src_layout[h].elems;
+            const uint64_t se = P.src_lay(h).elems;
             std::vector<uint64_t> sb = {se * 2, se * 4, se * 4, se * 4};
             std::vector<std::vector<Iv>> RW[4];
-            replay(rv, false, false, mask, grid, P.dst_layout[d].elems, sb, RW, A, true);
+            replay(rv, false, false, mask, grid, P.dst_lay(d).elems, sb, RW, A, true);
           }
         }
         for (int kk = 0; kk < 4; ++kk) {
           if (!(mask & (1u << kk))) continue;
           const int es = kk ? 4 : 2;
           std::vector<Iv> want;
-          for (auto& q : P.dst_layout[d].pieces) want.push_back({q.off * es, (q.off + q.elems()) * es});
+          for (auto& q : P.dst_lay(d).pieces) want.push_back({q.off * es, (q.off + q.elems()) * es});
           merge_equal(A[kk], want, std::string(name) + " unpack d" + std::to_string(d));
         }
       }
