@@ -198,3 +198,35 @@ def test_dp_errors():
     with pytest.raises(etc.EtcError) as e:
         etc.etc_plan(m, w, w, flags=HOST, failed=[4])
     assert e.value.code == etc.ERR_INVALID_ARG
+
+
+def test_large_dp_plan_repeats_one_replica():
+    """Llama-70B TP8xPP8 -> TP8xPP4 at DP 256 (16384 -> 8192 ranks): with no
+    failed rank, replica r migrates exactly as replica 0 does at DP 1, shifted
+    by r replicas (Sec. III-C: replicas are isolated), for the sketch and the
+    layouts; a plan this size builds in well under a second."""
+    import time
+    w = WORKLOADS["llama-70b"]
+    a1, b1 = w.src, w.dst
+    dp = 256
+    a, b = P(a1.tp, a1.pp, dp), P(b1.tp, b1.pp, dp)
+    t0 = time.perf_counter()
+    big = etc.etc_plan(w.model, a, b, rank=0, flags=HOST | etc.PLAN_SKETCH)
+    assert time.perf_counter() - t0 < 5.0
+    one = etc.etc_plan(w.model, a1, b1, flags=HOST | etc.PLAN_SKETCH)
+    Sr, Dr = a1.world, b1.world
+    pair1, pair = one.pairing(), big.pairing()
+    for r in (0, 1, 137, dp - 1):
+        want = np.where(pair1 >= 0, pair1 + r * Sr, -1)
+        np.testing.assert_array_equal(pair[r * Dr:(r + 1) * Dr], want)
+        for s1 in (0, 9, Sr - 1):
+            cnt, mb, dsp, tot = big.send_layout(r * Sr + s1)
+            c1, m1, d1, t1 = one.send_layout(s1)
+            np.testing.assert_array_equal(cnt[r * Dr:(r + 1) * Dr], c1)
+            np.testing.assert_array_equal(mb[r * Dr:(r + 1) * Dr], m1)
+            assert int(cnt.sum()) == int(c1.sum()) and tot == t1
+        for d1 in (0, 5, Dr - 1):
+            rc = big.recv_counts(r * Dr + d1)
+            np.testing.assert_array_equal(rc[r * Sr:(r + 1) * Sr], one.recv_counts(d1))
+            assert int(rc.sum()) == int(one.recv_counts(d1).sum())
+            assert big.arena_elems(etc.SIDE_DST, r * Dr + d1) == one.arena_elems(etc.SIDE_DST, d1)
