@@ -21,6 +21,7 @@
  *   etc_sketch       host: the migration sketch (pairing of new and old ranks)
  *   etc_plan         host: layouts, routing, message layout, tile tables
  *   etc_plan_defrag  host: virtual rank allocator and the coalesced pairing
+ *   etc_plan_message, etc_plan_refer   host: the instruction lists
  *   etc_cost_matrix  device: byte matrices over every (source, target) pair
  *   etc_pack         device: a source rank's shards -> one message per peer
  *   etc_unpack       device: received messages -> the target rank's shards
@@ -285,6 +286,39 @@ ETC_API int etc_plan_send_layout(const etc_plan_t* plan, int src_rank, uint64_t*
 
 /* counts[s] = bytes target d receives from source s (= ROUTE[s][d]); S entries. */
 ETC_API int etc_plan_recv_counts(const etc_plan_t* plan, int dst_rank, uint64_t* counts);
+
+/* One migration instruction (Sec. III-D: source, target, workload; all four
+ * state kinds move together): a box of a logical tensor, row-major in
+ * full-tensor coordinates, copied from the source rank's arenas to the target
+ * rank's.  Offsets are in elements and the same in the four arenas of a rank
+ * (and in the four kind sections of a message). */
+typedef struct {
+  int32_t tensor;          /* logical tensor (as etc_piece_info.tensor)           */
+  int32_t role;            /* copy role of the target's piece (1: tied duplicate) */
+  int64_t r0, r1, c0, c1;  /* the box: rows [r0, r1), columns [c0, c1)            */
+  uint64_t src_offset;     /* element offset of the box's first element, source  */
+  uint64_t src_ld;         /* row stride of the source piece, elements           */
+  uint64_t dst_offset;     /* element offset of the box's first element, target  */
+  uint64_t dst_ld;         /* row stride of the target piece, elements           */
+  uint64_t msg_offset;     /* element offset inside each kind section of the
+                              message; ETC_NO_MESSAGE for a Refer instruction   */
+} etc_instruction;
+#define ETC_NO_MESSAGE UINT64_MAX
+
+/* The instruction list of message src_rank -> dst_rank (Send on the source,
+ * Recv on the target), in message order; empty when nothing is routed.
+ * *count = number of instructions; out (host, may be NULL) receives the first
+ * min(cap, *count) of them.  Host only.  Errors: INVALID_ARG, RANK. */
+ETC_API int etc_plan_message(const etc_plan_t* plan, int src_rank, int dst_rank, etc_instruction* out,
+                             int cap, int* count);
+
+/* The Refer instructions of dst_rank: what its paired source keeps, which
+ * etc_refer copies arena to arena when the plan has ETC_PLAN_DIRECT_REFER
+ * (source offsets are in the paired source's arenas); empty otherwise (the
+ * kept part then travels in the paired source's message).  Same conventions
+ * as etc_plan_message. */
+ETC_API int etc_plan_refer(const etc_plan_t* plan, int dst_rank, etc_instruction* out, int cap,
+                           int* count);
 
 /* Compute one S x D (or D x S for ETC_CM_COST) uint64 matrix, row-major, into
  * device memory d_out, with one GPU kernel over every (source, target) pair

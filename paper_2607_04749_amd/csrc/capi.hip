@@ -11,6 +11,7 @@
 #include "etc.h"
 #include "etc_internal.hpp"
 #include "plan.hpp"
+#include "route.hpp"
 
 namespace {
 
@@ -176,6 +177,31 @@ int check_arenas(const void* const* arenas, const char* what) {
       return fail(ETC_ERR_ALIGN, std::string(what) + "[" + std::to_string(k) + "] is not 256-byte aligned");
   }
   return ETC_OK;
+}
+
+// The instruction of box b routed from source rank s (its arenas) to target
+// rank d; msg_offset as given.
+etc_instruction make_instruction(const etc_plan_t* P, int s, int d, const etc_plan_s::MsgBox& b,
+                                 uint64_t msg_offset) {
+  using namespace etc;
+  const int role_s = role_on(P->route_tensors[size_t(b.tensor)].src_stage, P->src.pp_of(s));
+  const RankLayout& Ls = P->src_lay(s);
+  const RankLayout& Ld = P->dst_lay(d);
+  const Piece& p = Ls.pieces[size_t(Ls.piece_of_tensor[role_s][size_t(b.tensor)])];
+  const Piece& q = Ld.pieces[size_t(Ld.piece_of_tensor[b.role_d][size_t(b.tensor)])];
+  etc_instruction x{};
+  x.tensor = b.tensor;
+  x.role = b.role_d;
+  x.r0 = b.r0;
+  x.r1 = b.r1;
+  x.c0 = b.c0;
+  x.c1 = b.c1;
+  x.src_offset = p.off + uint64_t((b.r0 - p.r0) * p.ld() + (b.c0 - p.c0));
+  x.src_ld = uint64_t(p.ld());
+  x.dst_offset = q.off + uint64_t((b.r0 - q.r0) * q.ld() + (b.c0 - q.c0));
+  x.dst_ld = uint64_t(q.ld());
+  x.msg_offset = msg_offset;
+  return x;
 }
 
 }  // namespace
@@ -398,6 +424,30 @@ int etc_plan_recv_counts(const etc_plan_t* P, int d, uint64_t* counts) {
     const etc_plan_s::Message& m = P->msgs[P->dst_msgs[k]];
     counts[m.s] = m.elems * 14;
   }
+  return ETC_OK;
+}
+
+int etc_plan_message(const etc_plan_t* P, int s, int d, etc_instruction* out, int cap, int* count) {
+  int rc = check_side_rank(P, ETC_SIDE_SRC, s);
+  if (rc) return rc;
+  if ((rc = check_side_rank(P, ETC_SIDE_DST, d))) return rc;
+  if (!count || cap < 0) return fail(ETC_ERR_INVALID_ARG, "count is NULL or cap is negative");
+  const etc_plan_s::Message* m = P->find_msg(s, d);
+  const size_t n = m ? m->boxes.size() : 0;
+  *count = int(n);
+  for (size_t i = 0; out && i < n && i < size_t(cap); ++i)
+    out[i] = make_instruction(P, s, d, m->boxes[i], m->boxes[i].moff);
+  return ETC_OK;
+}
+
+int etc_plan_refer(const etc_plan_t* P, int d, etc_instruction* out, int cap, int* count) {
+  int rc = check_side_rank(P, ETC_SIDE_DST, d);
+  if (rc) return rc;
+  if (!count || cap < 0) return fail(ETC_ERR_INVALID_ARG, "count is NULL or cap is negative");
+  const auto& boxes = P->refer[size_t(d)];
+  *count = int(boxes.size());
+  for (size_t i = 0; out && i < boxes.size() && i < size_t(cap); ++i)
+    out[i] = make_instruction(P, P->home[size_t(d)], d, boxes[i], ETC_NO_MESSAGE);
   return ETC_OK;
 }
 

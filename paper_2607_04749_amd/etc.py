@@ -57,6 +57,17 @@ class PieceInfo(ctypes.Structure):
                 ("c1", ctypes.c_int64), ("elem_offset", ctypes.c_uint64)]
 
 
+class Instruction(ctypes.Structure):
+    _fields_ = [("tensor", ctypes.c_int32), ("role", ctypes.c_int32),
+                ("r0", ctypes.c_int64), ("r1", ctypes.c_int64), ("c0", ctypes.c_int64),
+                ("c1", ctypes.c_int64), ("src_offset", ctypes.c_uint64), ("src_ld", ctypes.c_uint64),
+                ("dst_offset", ctypes.c_uint64), ("dst_ld", ctypes.c_uint64),
+                ("msg_offset", ctypes.c_uint64)]
+
+
+NO_MESSAGE = (1 << 64) - 1
+
+
 class EtcError(RuntimeError):
     def __init__(self, code, func, msg):
         super().__init__(f"{func} failed ({code}): {msg}")
@@ -104,6 +115,8 @@ def _load():
     L.etc_plan_chunk_layout.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, u64p]
     L.etc_pack_kind.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, vp]
     L.etc_unpack_kind.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, vp]
+    L.etc_plan_message.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, ctypes.c_int, i32p]
+    L.etc_plan_refer.argtypes = [vp, ctypes.c_int, vp, ctypes.c_int, i32p]
     L.etc_last_error.argtypes = []
     L.etc_last_error.restype = ctypes.c_char_p
     if len(hip_runtimes()) > 1:
@@ -214,6 +227,22 @@ class Plan:
                                          dsp.ctypes.data, ctypes.byref(tot)),
                "etc_plan_send_layout")
         return cnt, mb, dsp, tot.value
+
+    def _instructions(self, call, *args):
+        n = ctypes.c_int()
+        _check(call(self.handle, *args, None, 0, ctypes.byref(n)), call.__name__)
+        arr = (Instruction * max(n.value, 1))()
+        _check(call(self.handle, *args, ctypes.cast(arr, ctypes.c_void_p), n.value, ctypes.byref(n)),
+               call.__name__)
+        return [{f: getattr(x, f) for f, _ in Instruction._fields_} for x in arr[:n.value]]
+
+    def message(self, s, d):
+        """Instruction list of message s -> d (dicts with the etc_instruction fields)."""
+        return self._instructions(_lib.etc_plan_message, s, d)
+
+    def refer(self, d):
+        """Refer instructions of target d (ETC_PLAN_DIRECT_REFER plans)."""
+        return self._instructions(_lib.etc_plan_refer, d)
 
     def refer_bytes(self, d):
         """Bytes etc_refer copies for target d (ETC_PLAN_DIRECT_REFER plans)."""
