@@ -27,6 +27,10 @@
  *   etc_unpack       device: received messages -> the target rank's shards
  *   etc_pack_kind,   device: the same, one state kind at a time (state
  *   etc_unpack_kind          chunking)
+ *   etc_refer,       device: what a target's paired source keeps, arena to
+ *   etc_refer_kind           arena (Refer), all kinds or one
+ *   etc_plan_* queries      host: dimensions, pieces, arena sizes, send and
+ *                            chunk layouts, receive counts, pairing, roles
  * Moving messages between GPUs is the caller's business (a grouped
  * send/recv or all-to-all-v with the counts from etc_plan_send_layout).
  *
