@@ -31,3 +31,21 @@ def test_random_full_emulation(i):
     say("random case", i, m, a, "->", b)
     full_compare(m, a, b, 0x5EED + i)
     full_compare(m, a, b, 0x5EED + i, pair=sk, round_trip=False)
+
+
+DP_FAIL_CASES = [c for c in cases(200, base=0xD9) if c[1].dp > 1][:8]
+
+
+@pytest.mark.parametrize("i", range(len(DP_FAIL_CASES)))
+def test_random_failed_rank_full_emulation(i):
+    """Random configurations with two source replicas and one failed source
+    rank (always recoverable from the other replica): every byte against the
+    oracle, under the identity pairing and under the sketch with direct Refer."""
+    m, a, b = DP_FAIL_CASES[i]
+    failed = [int(np.random.default_rng(0xFA + i).integers(0, a.world))]
+    say("random failed-rank case", i, m, a, "->", b, "failed", failed)
+    full_compare(m, a, b, 0xFA11 + i, failed=failed)
+    C = oracle.matrices(m, a, b, failed=failed)["cost"]
+    sk, _ = oracle.sketch(C)
+    sk = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)], np.int32)
+    full_compare(m, a, b, 0xFA11 + i, pair=sk, failed=failed, round_trip=False, direct_refer=True)

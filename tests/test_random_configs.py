@@ -57,3 +57,32 @@ def test_random_case(i):
         for d in range(b.world):
             np.testing.assert_array_equal(p.recv_counts(d), R[:, d])
         p.free()
+
+
+DP_FAIL = [c for c in cases(200, base=0xD9) if c[1].dp > 1][:24]
+
+
+@pytest.mark.parametrize("i", range(len(DP_FAIL)))
+def test_random_failed_rank_plans(i):
+    """Random configurations with two source replicas and one failed source
+    rank: the planner's message layouts and routing equal the oracle's, and
+    every target still receives exactly its bytes."""
+    m, a, b = DP_FAIL[i]
+    failed = [int(np.random.default_rng(0xFA + i).integers(0, a.world))]
+    for pair in (None, "sketch"):
+        if pair == "sketch":
+            C = oracle.matrices(m, a, b, failed=failed)["cost"]
+            sk, _ = oracle.sketch(C)
+            pair = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)],
+                            np.int32)
+        p = etc.etc_plan(m, a, b, flags=HOST, pair=pair, failed=failed)
+        R = oracle.matrices(m, a, b, pair=pair, failed=failed)["route"]
+        assert not R[failed[0]].any()
+        for s in range(a.world):
+            got, want = p.send_layout(s), oracle.send_layout(m, a, b, s, pair=pair, failed=failed)
+            for g, o in zip(got, want):
+                np.testing.assert_array_equal(g, o)
+        for d in range(b.world):
+            np.testing.assert_array_equal(p.recv_counts(d), R[:, d])
+            assert int(R[:, d].sum()) == dp_bytes(m, b, d)
+        p.free()
