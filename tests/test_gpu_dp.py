@@ -67,3 +67,19 @@ def test_tiny_gpt_dp_scale_out_and_failures():
     full_compare(w.model, P(2, 2, 1), P(4, 1, 2), w.seed)
     say("tiny-gpt DP2 with failed ranks 0 and 5")
     full_compare(w.model, P(2, 2, 2), P(4, 1, 1), w.seed, failed=[0, 5])
+
+
+def test_large_dp_cost_matrices():
+    """Llama-70B TP8xPP8 DP4 -> TP8xPP4 DP2 (256 x 64 cells) with two failed
+    source ranks in different replicas: all four device matrices equal the
+    oracle's, under the sketch and under the identity pairing."""
+    from gpu_util import check_matrices
+    from paper_2607_04749_amd.workloads import WORKLOADS, Parallel
+    w = WORKLOADS["llama-70b"]
+    a, b = Parallel(8, 8, 4), Parallel(8, 4, 2)
+    failed = [3, 70]
+    say("llama-70b DP4 -> DP2 with failed ranks", failed, ": device matrices vs oracle")
+    sk = etc.etc_plan(w.model, a, b, flags=etc.PLAN_SKETCH, failed=failed)
+    check_matrices(sk, w.model, a, b, pair=sk.pairing(), failed=failed)
+    ident = etc.etc_plan(w.model, a, b, failed=failed)
+    check_matrices(ident, w.model, a, b, pair=None, failed=failed)
