@@ -40,5 +40,35 @@ def test_traffic_record_matches_the_kernel():
 @pytest.mark.parametrize("pairing", ["identity", "sketch"])
 def test_cpu_baseline_runs(pairing):
     out = bench.cpu_baseline(WORKLOADS["tiny-gpt"], pairing)
-    assert out["kind"] == "oracle" and out["cores"] == 1 and out["unit"] == "GB/s"
-    assert out["value"] > 0 and "layers 0-3" in out["sample"]
+    assert out["kind"] == "oracle" and out["cores"] == min(16, bench.host_threads()) and out["unit"] == "GB/s"
+    assert out["value"] > 0 and "layers 0-3" in out["sample"] and "on one thread" in out["sample"]
+
+
+def test_oracle_threads_write_the_same_bytes():
+    """cpu_baseline runs the oracle one tensor per thread: that must write
+    exactly what one call over all tensors writes."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import oracle
+    from helpers import empty_arenas, host_arenas
+    w = WORKLOADS["tiny-gpt"]
+    m, a, b = w.model, w.src, w.dst
+    hs = host_arenas(m, a, range(a.world), w.seed)
+    outs = []
+    for threaded in (False, True):
+        hd = empty_arenas(m, b, range(b.world))
+        hb = {s: np.zeros(oracle.send_layout(m, a, b, s)[3], np.uint8) for s in range(a.world)}
+        if threaded:
+            nt = len(oracle.tensors(m))
+            with ThreadPoolExecutor(8) as ex:
+                list(ex.map(lambda t: oracle.migrate(m, a, b, hs, hd, hb, t, t + 1), range(nt)))
+        else:
+            oracle.migrate(m, a, b, hs, hd, hb)
+        outs.append((hd, hb))
+    (d1, b1), (d2, b2) = outs
+    for d in d1:
+        for k in range(4):
+            assert np.array_equal(d1[d][k], d2[d][k])
+    for s in b1:
+        assert np.array_equal(b1[s], b2[s])
