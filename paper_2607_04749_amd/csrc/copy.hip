@@ -6,21 +6,29 @@
 // source rank's arenas into a target rank's.  Boxes are pre-cut on the host
 // into uniform tiles of kTileElems elements per kind.
 //
-// Launch shape: a persistent grid of one 256-thread workgroup per CU (the
-// launcher reserves just over half of a CU's LDS per workgroup, so no second
-// workgroup can become resident), walking tiles interleaved round by round
-// over the grid, each XCD taking a contiguous run of every round
-// (first_tile), so the whole GPU sweeps the buffers front to back.
-// A tile's descriptor is uniform across the workgroup (scalar loads).
-// Within a tile, each thread moves 16-byte vectors in batches: 16 loads in
-// flight, then the 16 stores, for contiguous rows (a workgroup streams 64 KB
-// per batch); 8, predicated, for strided rows.  Loads and stores are non-temporal since
-// nothing is reused.  On MI355X this shape measured best of the ones tried
-// (deeper batches at low occupancy beat more resident waves with shallow
-// batches: the memory system is saturated and fewer, larger contiguous
-// request streams per CU use it better).  A launch of a single state kind
-// (state chunking) also batches the shorter 2-byte rows 8 deep; a launch of
-// all four kinds does not, which measured faster there.
+// Two launch shapes, chosen by what a launch copies:
+//
+// All four kinds (pack, unpack, Refer): one short-lived workgroup per
+// sub-chunk of a tile, kSubPerTile per tile and kSubElems elements of each
+// kind per sub-chunk (4 KB of each fp32 kind, one 16-byte vector per thread;
+// 2 KB of bf16), the kinds copied one after another.  The hardware dispatches
+// the workgroups in index order, so the whole GPU advances through each
+// buffer as one compact front, and keeps as many of them resident as the
+// register budget allows (eight per CU).  On MI355X this ran 3-11 % faster
+// than a persistent grid on every share measured, and it holds its rate
+// where the persistent kernel loses about 10 % to an unfavourable relative
+// placement of the source and target buffers.
+//
+// One kind (state chunking): a persistent grid of one 256-thread workgroup
+// per CU (the launcher reserves just over half of a CU's LDS per workgroup,
+// so no second workgroup can become resident), walking tiles interleaved
+// round by round over the grid, each XCD taking a contiguous run of every
+// round (first_tile).  Within a tile each thread moves 16-byte vectors in
+// batches: 16 loads in flight, then the 16 stores, for contiguous rows
+// (8 deep for the shorter bf16 rows); 8, predicated, for strided rows.
+//
+// A tile's descriptor is uniform across the workgroup (scalar loads).  Loads
+// and stores are non-temporal since nothing is reused.
 #include <hip/hip_runtime.h>
 
 #include "copy_geom.hpp"
@@ -42,13 +50,89 @@ struct CopyArgs {
   char* peer[ETC_MAX_PEERS];  // start of each peer's message (kMsgArenas: source arena of kind k)
 };
 
+// One kind of one tile: where the copy reads and writes, and the row pitches.
+template <bool kPack, int kKind>
+struct KindTile {
+  static constexpr int es = kKind == 0 ? 2 : 4;
+  using E = typename std::conditional<es == 2, uint16_t, uint32_t>::type;
+  char* Mb;  // this kind's section of the message, or (Refer) the source arena of this kind
+  const char* src;
+  char* dst;
+  uint64_t sld, dld;  // row pitches in bytes
+  __device__ __forceinline__ KindTile(const CopyArgs& a, const CopyBox& b, char* mbase, const TileGeom& g) {
+    char* A = a.arena[kKind] + tile_arena_elem(b, g) * es;
+    Mb = a.mode == kMsgArenas ? a.peer[kKind]
+                              : mbase + (a.mode == kMsgSections ? section_byte(b.msg_npad, kKind) : 0);
+    char* M = Mb + tile_msg_elem(b, g) * es;
+    src = kPack ? A : M;
+    dst = kPack ? M : A;
+    sld = (kPack ? uint64_t(b.a_ld) : b.m_ld) * es;
+    dld = (kPack ? b.m_ld : uint64_t(b.a_ld)) * es;
+  }
+  // zero the padding that rounds the box up to a multiple of 8 elements
+  __device__ __forceinline__ void zero_pad(const CopyBox& b) const {
+    E* tail = reinterpret_cast<E*>(Mb + (b.m_off + uint64_t(b.rows) * b.cols) * es);
+    if (threadIdx.x < b.pad) tail[threadIdx.x] = 0;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// All four kinds: one workgroup per sub-chunk.
+
+template <bool kPack, int kKind>
+__device__ __forceinline__ void copy_sub_kind(const CopyArgs& a, const CopyBox& b, char* mbase,
+                                              const TileGeom& g, uint32_t j) {
+  using KT = KindTile<kPack, kKind>;
+  using E = typename KT::E;
+  constexpr int es = KT::es;
+  const KT k(a, b, mbase, g);
+  uint32_t lo, hi;
+  if (sub_vectors(b, g, es)) {
+    constexpr uint32_t vw = 16 / es;
+    const uint32_t vpr = g.nc / vw;
+    sub_range(j, kSubElems / vw, g.nr * vpr, &lo, &hi);
+    const uint32_t i = lo + threadIdx.x;
+    if (i < hi) {
+      const uint32_t r = g.nr == 1 ? 0 : i / vpr;
+      const uint32_t c = i - r * vpr;
+      __builtin_nontemporal_store(
+          __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k.src + r * k.sld + uint64_t(c) * 16)),
+          reinterpret_cast<u32x4*>(k.dst + r * k.dld + uint64_t(c) * 16));
+    }
+  } else {
+    sub_range(j, kSubElems, g.nr * g.nc, &lo, &hi);
+    const E* S = reinterpret_cast<const E*>(k.src);
+    E* D = reinterpret_cast<E*>(k.dst);
+    for (uint32_t i = lo + threadIdx.x; i < hi; i += kCopyThreads) {
+      const uint32_t r = i / g.nc, c = i - r * g.nc;
+      D[r * (k.dld / es) + c] = S[r * (k.sld / es) + c];
+    }
+  }
+  if (kPack && j == 0 && g.last && b.pad) k.zero_pad(b);
+}
+
+template <bool kPack>
+__global__ __launch_bounds__(kCopyThreads) void copy_sub_kernel(CopyArgs a) {
+  const uint32_t t = blockIdx.x / kSubPerTile, j = blockIdx.x % kSubPerTile;
+  const uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
+  const CopyBox b = a.boxes[bi];
+  const TileGeom g = tile_geom(b, t, a.boxes[bi + 1].tile0);
+  char* mbase = a.peer[b.peer];
+  copy_sub_kind<kPack, 0>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 1>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 2>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 3>(a, b, mbase, g, j);
+}
+
+// ---------------------------------------------------------------------------
+// One kind: a persistent grid.
+
 constexpr int kRowBatch = 16;  // vectors in flight per thread, contiguous rows
+constexpr int kRowBatch2 = 8;  // then the rest of a contiguous row (a bf16 tile is 8 vectors per thread)
 constexpr int kBatch2D = 8;    // vectors in flight per thread, strided rows (predicated)
 
 // Copy nr rows of row_bytes bytes (16-byte aligned starts, row_bytes a
 // multiple of 16 when nr > 1) from src (row pitch sld bytes) to dst (pitch dld).
-// kSingle: the launch copies one state kind only.
-template <bool kSingle>
 __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64_t sld,
                                             char* __restrict__ dst, uint64_t dld, uint32_t nr,
                                             uint32_t row_bytes) {
@@ -67,18 +151,16 @@ __device__ __forceinline__ void copy_vec_2d(const char* __restrict__ src, uint64
         __builtin_nontemporal_store(
             v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
     }
-    if (kSingle) {
-      for (; i + 7 * kCopyThreads < nv; i += 8 * kCopyThreads) {
-        u32x4 v[8];
+    for (; i + (kRowBatch2 - 1) * kCopyThreads < nv; i += kRowBatch2 * kCopyThreads) {
+      u32x4 v[kRowBatch2];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          v[u] = __builtin_nontemporal_load(
-              reinterpret_cast<const u32x4*>(src + uint64_t(i + u * kCopyThreads) * 16));
+      for (int u = 0; u < kRowBatch2; ++u)
+        v[u] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(src + uint64_t(i + u * kCopyThreads) * 16));
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          __builtin_nontemporal_store(
-              v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
-      }
+      for (int u = 0; u < kRowBatch2; ++u)
+        __builtin_nontemporal_store(
+            v[u], reinterpret_cast<u32x4*>(dst + uint64_t(i + u * kCopyThreads) * 16));
     }
     for (; i < nv; i += kCopyThreads)
       __builtin_nontemporal_store(
@@ -122,41 +204,30 @@ __device__ __forceinline__ void copy_elems_2d(const E* __restrict__ src, uint64_
   }
 }
 
-template <bool kPack, int kKind, bool kSingle>
+template <bool kPack, int kKind>
 __device__ __forceinline__ void copy_tile_kind(const CopyArgs& a, const CopyBox& b, char* mbase,
                                                const TileGeom& g) {
-  constexpr int es = kKind == 0 ? 2 : 4;
-  using E = typename std::conditional<es == 2, uint16_t, uint32_t>::type;
-  char* A = a.arena[kKind] + tile_arena_elem(b, g) * es;
-  // this kind's section of the message, or (Refer) the source arena of this kind
-  char* Mb = a.mode == kMsgArenas ? a.peer[kKind]
-                                  : mbase + (a.mode == kMsgSections ? section_byte(b.msg_npad, kKind) : 0);
-  char* M = Mb + tile_msg_elem(b, g) * es;
-  const char* src = kPack ? A : M;
-  char* dst = kPack ? M : A;
-  const uint64_t sld = (kPack ? uint64_t(b.a_ld) : b.m_ld) * es;
-  const uint64_t dld = (kPack ? b.m_ld : uint64_t(b.a_ld)) * es;
+  using KT = KindTile<kPack, kKind>;
+  using E = typename KT::E;
+  constexpr int es = KT::es;
+  const KT k(a, b, mbase, g);
   const bool vec = (b.vec >> (es == 2 ? 0 : 1)) & 1;
   if (vec) {
     constexpr uint32_t vw = 16 / es;
     const uint32_t nvc = g.nr == 1 ? (g.nc / vw) * vw : g.nc;  // vector part of each row
-    copy_vec_2d<kSingle>(src, sld, dst, dld, g.nr, nvc * es);
+    copy_vec_2d(k.src, k.sld, k.dst, k.dld, g.nr, nvc * es);
     if (nvc < g.nc)
-      copy_elems_2d<E>(reinterpret_cast<const E*>(src), sld / es, reinterpret_cast<E*>(dst),
-                       dld / es, g.nr, nvc, g.nc);
+      copy_elems_2d<E>(reinterpret_cast<const E*>(k.src), k.sld / es, reinterpret_cast<E*>(k.dst),
+                       k.dld / es, g.nr, nvc, g.nc);
   } else {
-    copy_elems_2d<E>(reinterpret_cast<const E*>(src), sld / es, reinterpret_cast<E*>(dst),
-                     dld / es, g.nr, 0, g.nc);
+    copy_elems_2d<E>(reinterpret_cast<const E*>(k.src), k.sld / es, reinterpret_cast<E*>(k.dst),
+                     k.dld / es, g.nr, 0, g.nc);
   }
-  if (kPack && g.last && b.pad) {
-    // zero the padding that rounds the box up to a multiple of 8 elements
-    E* tail = reinterpret_cast<E*>(Mb + (b.m_off + uint64_t(b.rows) * b.cols) * es);
-    if (threadIdx.x < b.pad) tail[threadIdx.x] = 0;
-  }
+  if (kPack && g.last && b.pad) k.zero_pad(b);
 }
 
-template <bool kPack, bool kSingle>
-__global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
+template <bool kPack, int kKind>
+__device__ __forceinline__ void copy_walk(const CopyArgs& a) {
   uint32_t t = first_tile(blockIdx.x, gridDim.x);
   if (t >= a.ntiles) return;
   uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
@@ -168,12 +239,18 @@ __global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
       b = a.boxes[bi];
       next0 = a.boxes[bi + 1].tile0;
     }
-    const TileGeom g = tile_geom(b, t, next0);
-    char* mbase = a.peer[b.peer];
-    if (a.kind_mask & 1) copy_tile_kind<kPack, 0, kSingle>(a, b, mbase, g);
-    if (a.kind_mask & 2) copy_tile_kind<kPack, 1, kSingle>(a, b, mbase, g);
-    if (a.kind_mask & 4) copy_tile_kind<kPack, 2, kSingle>(a, b, mbase, g);
-    if (a.kind_mask & 8) copy_tile_kind<kPack, 3, kSingle>(a, b, mbase, g);
+    copy_tile_kind<kPack, kKind>(a, b, a.peer[b.peer], tile_geom(b, t, next0));
+  }
+}
+
+template <bool kPack>
+__global__ __launch_bounds__(kCopyThreads) void copy_kernel(CopyArgs a) {
+  switch (a.kind_mask) {
+    case 1: copy_walk<kPack, 0>(a); break;
+    case 2: copy_walk<kPack, 1>(a); break;
+    case 4: copy_walk<kPack, 2>(a); break;
+    case 8: copy_walk<kPack, 3>(a); break;
+    default: break;
   }
 }
 
@@ -183,6 +260,9 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
                        uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, MsgMode mode,
                        void* const arena[4], void* const* peers, int npeers, hipStream_t stream) {
   if (ntiles == 0 || kind_mask == 0) return hipSuccess;
+  const bool all = kind_mask == 0xFu;
+  const bool single = kind_mask < 16 && (kind_mask & (kind_mask - 1)) == 0;
+  if (!all && !single) return hipErrorInvalidValue;  // a launch copies all four kinds or one
   CopyArgs a{};
   a.boxes = boxes;
   a.nbox = nbox;
@@ -191,18 +271,22 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   a.mode = mode;
   for (int k = 0; k < 4; ++k) a.arena[k] = static_cast<char*>(arena[k]);
   for (int p = 0; p < npeers; ++p) a.peer[p] = static_cast<char*>(peers[p]);
+  if (all) {
+    const uint64_t nwg = uint64_t(ntiles) * kSubPerTile;
+    if (nwg > uint64_t(INT32_MAX)) return hipErrorInvalidValue;
+    if (pack)
+      hipLaunchKernelGGL((copy_sub_kernel<true>), dim3(uint32_t(nwg)), dim3(kCopyThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL((copy_sub_kernel<false>), dim3(uint32_t(nwg)), dim3(kCopyThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   const uint32_t g = grid < ntiles ? grid : ntiles;
   // the dynamic LDS is not used by the kernel: it caps residency at one
   // workgroup per CU
-  const bool single = (kind_mask & (kind_mask - 1)) == 0;
-  if (pack && single)
-    hipLaunchKernelGGL((copy_kernel<true, true>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
-  else if (pack)
-    hipLaunchKernelGGL((copy_kernel<true, false>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
-  else if (single)
-    hipLaunchKernelGGL((copy_kernel<false, true>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
+  if (pack)
+    hipLaunchKernelGGL((copy_kernel<true>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
   else
-    hipLaunchKernelGGL((copy_kernel<false, false>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
+    hipLaunchKernelGGL((copy_kernel<false>), dim3(g), dim3(kCopyThreads), lds_reserve, stream, a);
   return hipGetLastError();
 }
 

@@ -59,6 +59,29 @@ __host__ __device__ inline uint64_t tile_msg_elem(const CopyBox& b, const TileGe
   return b.m_off + uint64_t(g.r0) * b.m_ld + g.c0;
 }
 
+// Sub-chunks of the all-kinds launch: one workgroup per sub-chunk j of tile t
+// (kSubPerTile per tile).  For each kind, sub-chunk j covers the tile's
+// vectors [j * kSubElems / vw, (j + 1) * kSubElems / vw) when the kind moves
+// in 16-byte vectors of vw elements, else its elements
+// [j * kSubElems, (j + 1) * kSubElems), both in row-major order over the
+// tile and clipped to the tile's size.
+constexpr uint32_t kSubPerTile = 16;
+constexpr uint32_t kSubElems = kTileElems / kSubPerTile;  // 1024
+
+// Whether the kind of element size es moves a tile in 16-byte vectors: the
+// box is vector-aligned for that size and every row of the tile is whole
+// vectors (a ragged single-row tile goes element by element).
+__host__ __device__ inline bool sub_vectors(const CopyBox& b, const TileGeom& g, int es) {
+  return ((b.vec >> (es == 2 ? 0 : 1)) & 1) && g.nc % (16u / uint32_t(es)) == 0;
+}
+
+// Index range [lo, hi) of sub-chunk j over n items, per items per sub-chunk.
+__host__ __device__ inline void sub_range(uint32_t j, uint32_t per, uint32_t n, uint32_t* lo, uint32_t* hi) {
+  const uint32_t a = j * per;
+  *lo = a < n ? a : n;
+  *hi = a + per < n ? a + per : n;
+}
+
 // Byte offset of kind k's section inside a message of npad elements per section.
 __host__ __device__ inline uint64_t section_byte(uint64_t npad, int k) {
   return npad * (k == 0 ? 0 : (k == 1 ? 2 : (k == 2 ? 6 : 10)));

@@ -1,10 +1,12 @@
-// tilewalk.cpp -- host replay of the copy kernel's tile walk over the copy
-// tables the planner builds (pack, unpack and Refer; all kinds at once and
-// one kind at a time; any grid size).  For every tile it checks that each
-// row stays inside its arena, message section or source arena, that vector
-// accesses are 16-byte aligned, and that the writes of a launch cover the
-// target bytes exactly once: each message (padding included) for a pack,
-// each target piece for the unpack plus Refer of one target.
+// tilewalk.cpp -- host replay of the copy kernels' walks over the copy
+// tables the planner builds (pack, unpack and Refer; all kinds at once, one
+// workgroup per sub-chunk of a tile; one kind at a time, a persistent grid of
+// any size).  For every tile it checks that each row stays inside its arena,
+// message section or source arena, that vector accesses are 16-byte aligned,
+// that a sub-chunk needs no more lanes than a workgroup has, and that the
+// writes of a launch cover the target bytes exactly once: each message
+// (padding included) for a pack, each target piece for the unpack plus Refer
+// of one target.
 //
 // Test code: it links the library's host planner and its tile geometry
 // header; it computes no expected values.
@@ -45,6 +47,74 @@ static uint64_t npad_of(const etc_plan_t& P, int s, int d) {
   return m ? m->npad : 0;
 }
 
+// Sort and merge one tile's write intervals, failing on any overlap.
+static std::vector<Iv> merge_tile(std::vector<Iv> w, const char* what) {
+  std::sort(w.begin(), w.end(), [](Iv a, Iv b) { return a.lo < b.lo; });
+  std::vector<Iv> m;
+  for (auto x : w) {
+    if (x.hi == x.lo) continue;
+    if (!m.empty() && x.lo < m.back().hi) { FAIL("%s: sub-chunks of one tile overlap", what); continue; }
+    if (!m.empty() && m.back().hi == x.lo) m.back().hi = x.hi; else m.push_back(x);
+  }
+  return m;
+}
+
+// Replay an all-kinds launch as the sub-chunk kernel runs it: workgroup
+// t * kSubPerTile + j copies sub-chunk j of every kind of tile t.
+static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint64_t arena_elems,
+                       const std::vector<uint64_t>& peer_bytes, std::vector<std::vector<Iv>> W[4],
+                       std::vector<Iv> A[4], bool arenas) {
+  const uint32_t nbox = uint32_t(v.size() - 1), ntiles = v.back().tile0;
+  if (uint64_t(ntiles) * kSubPerTile > uint64_t(INT32_MAX)) { FAIL("grid over 2^31 - 1 workgroups"); return; }
+  for (uint32_t t = 0; t < ntiles; ++t) {
+    const uint32_t bi = box_of_tile(v.data(), nbox, t);  // the same for every j of the tile
+    if (bi >= nbox) { FAIL("tile past last box"); return; }
+    const CopyBox& b = v[bi];
+    const TileGeom g = tile_geom(b, t, v[bi + 1].tile0);
+    if (g.nr == 0 || g.nc == 0 || g.r0 >= b.rows || g.c0 >= b.cols) FAIL("empty/outside tile");
+    if (!arenas && b.peer >= peer_bytes.size()) { FAIL("peer slot %u out of range", b.peer); return; }
+    for (int k = 0; k < 4; ++k) {
+      const int es = k == 0 ? 2 : 4;
+      const uint64_t ae = tile_arena_elem(b, g), me = tile_msg_elem(b, g);
+      const uint64_t sec = (sectioned && !arenas) ? section_byte(b.msg_npad, k) : 0;
+      const uint64_t sec_end = arenas ? peer_bytes[k] : sec + b.msg_npad * es;
+      const uint64_t sp = (pack ? uint64_t(b.a_ld) : b.m_ld) * es, dp = (pack ? b.m_ld : uint64_t(b.a_ld)) * es;
+      if (!arenas && b.m_ld != b.cols) FAIL("message box with a row stride");
+      if (arenas && (b.pad || b.msg_npad)) FAIL("refer box with padding");
+      if (std::max(sp, dp) * (g.nr - 1) + uint64_t(g.nc) * es >= (1ull << 31)) FAIL("tile extent over 2^31");
+      const bool vk = sub_vectors(b, g, es);
+      const uint32_t unit = vk ? 16u / uint32_t(es) : 1u;  // elements per item
+      const uint32_t per = kSubElems / unit;               // items per sub-chunk
+      const uint32_t ipr = g.nc / unit;                    // items per row
+      if (vk && per > uint32_t(kCopyThreads)) FAIL("a vector sub-chunk needs more lanes than threads");
+      if (vk && g.nc % unit) FAIL("vector rows not whole vectors");
+      std::vector<Iv> tw;
+      for (uint32_t j = 0; j < kSubPerTile; ++j) {
+        uint32_t lo, hi;
+        sub_range(j, per, g.nr * ipr, &lo, &hi);
+        for (uint32_t r = lo / (ipr ? ipr : 1); lo < hi && r <= (hi - 1) / ipr; ++r) {
+          const uint32_t c0 = std::max(lo, r * ipr) - r * ipr, c1 = std::min(hi, (r + 1) * ipr) - r * ipr;
+          const uint64_t abase = (ae + uint64_t(r) * b.a_ld) * es, mbase = sec + (me + uint64_t(r) * b.m_ld) * es;
+          const uint64_t alo = abase + uint64_t(c0) * unit * es, ahi = abase + uint64_t(c1) * unit * es;
+          const uint64_t mlo = mbase + uint64_t(c0) * unit * es, mhi = mbase + uint64_t(c1) * unit * es;
+          if (ahi > arena_elems * es) FAIL("arena OOB kind %d", k);
+          if ((!arenas && mhi > peer_bytes[b.peer]) || mhi > sec_end) FAIL("message OOB peer %u kind %d", b.peer, k);
+          if (vk && (abase % 16 || mbase % 16)) FAIL("vector misaligned kind %d", k);
+          tw.push_back(pack ? Iv{mlo, mhi} : Iv{alo, ahi});
+        }
+      }
+      if (pack && g.last && b.pad) {
+        const uint64_t plo = sec + (b.m_off + uint64_t(b.rows) * b.cols) * es, phi = plo + uint64_t(b.pad) * es;
+        if (phi > sec_end) FAIL("pad overrun");
+        tw.push_back({plo, phi});
+      }
+      for (auto x : merge_tile(tw, "sub-chunk walk")) {
+        if (pack) W[k][b.peer].push_back(x); else A[k].push_back(x);
+      }
+    }
+  }
+}
+
 // Replay one launch exactly as the kernel walks it.  peer_bytes[p] = length of
 // peer p's message; W[k][p] collects message writes (pack), A[k] arena writes.
 static void replay(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask, uint32_t G,
@@ -52,6 +122,11 @@ static void replay(const std::vector<CopyBox>& v, bool pack, bool sectioned, uin
                    std::vector<std::vector<Iv>> W[4], std::vector<Iv> A[4], bool arenas = false) {
   const uint32_t nbox = uint32_t(v.size() - 1), ntiles = v.back().tile0;
   if (ntiles == 0) return;
+  if (kind_mask == 0xFu) {
+    replay_sub(v, pack, sectioned, arena_elems, peer_bytes, W, A, arenas);
+    return;
+  }
+  if (kind_mask & (kind_mask - 1)) { FAIL("a launch of more than one kind but not all four"); return; }
   G = G < ntiles ? G : ntiles;
   for (uint32_t bid = 0; bid < G; ++bid) {
     uint32_t t = first_tile(bid, G);
