@@ -111,7 +111,10 @@ enum MsgMode : uint32_t {
 };
 
 // kernel launchers (copy.hip, cost.hip)
-// kind_mask: kinds to copy (bit k)
+// kind_mask: kinds to copy (bit k): all four (one workgroup per tile
+// sub-chunk; grid and lds_reserve unused) or one (persistent grid of `grid`
+// workgroups, each reserving lds_reserve bytes of LDS); any other mask is
+// hipErrorInvalidValue
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
                        uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, MsgMode mode,
                        void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
@@ -184,8 +187,8 @@ struct etc_plan_s {
 
   // device side
   int device = -1;
-  uint32_t copy_grid = 0;       // persistent copy grid: one workgroup per CU
-  uint32_t copy_lds_reserve = 0;  // dynamic LDS per copy workgroup (occupancy cap)
+  uint32_t copy_grid = 0;       // one-kind copy launches: persistent grid, one workgroup per CU
+  uint32_t copy_lds_reserve = 0;  // dynamic LDS per one-kind copy workgroup (occupancy cap)
   etc::RouteTensor* d_route_tensors = nullptr;
   int32_t* d_home = nullptr;  // device copy of home (D entries)
   uint32_t* d_failed = nullptr;  // device copy of failed_bits
