@@ -8,16 +8,15 @@
 //
 // Two launch shapes, chosen by what a launch copies:
 //
-// All four kinds (pack, unpack, Refer): one short-lived workgroup per
-// sub-chunk of a tile, kSubPerTile per tile and kSubElems elements of each
-// kind per sub-chunk (4 KB of each fp32 kind, one 16-byte vector per thread;
-// 2 KB of bf16), the kinds copied one after another.  The hardware dispatches
-// the workgroups in index order, so the whole GPU advances through each
-// buffer as one compact front, and keeps as many of them resident as the
-// register budget allows (eight per CU).  On MI355X this ran 3-11 % faster
-// than a persistent grid on every share measured, and it holds its rate
-// where the persistent kernel loses about 10 % to an unfavourable relative
-// placement of the source and target buffers.
+// All four kinds (pack, unpack, Refer): one short-lived one-wavefront
+// workgroup per sub-chunk of a tile, kSubPerTile per tile and kSubElems
+// elements of each kind per sub-chunk (1 KB of each fp32 kind, one 16-byte
+// vector per lane; 512 B of bf16), the kinds copied one after another.  The
+// hardware dispatches the workgroups in index order, so the whole GPU
+// advances through each buffer as one compact front.  On MI355X this ran
+// 5-14 % faster than a persistent grid on every share measured, and it holds
+// its rate where the persistent kernel loses about 10 % to an unfavourable
+// relative placement of the source and target buffers.
 //
 // One kind (state chunking): a persistent grid of one 256-thread workgroup
 // per CU (the launcher reserves just over half of a CU's LDS per workgroup,
@@ -91,7 +90,7 @@ __device__ __forceinline__ void copy_sub_kind(const CopyArgs& a, const CopyBox& 
     constexpr uint32_t vw = 16 / es;
     const uint32_t vpr = g.nc / vw;
     sub_range(j, kSubElems / vw, g.nr * vpr, &lo, &hi);
-    const uint32_t i = lo + threadIdx.x;
+    const uint32_t i = lo + threadIdx.x;  // at most one vector per lane
     if (i < hi) {
       const uint32_t r = g.nr == 1 ? 0 : i / vpr;
       const uint32_t c = i - r * vpr;
@@ -103,7 +102,7 @@ __device__ __forceinline__ void copy_sub_kind(const CopyArgs& a, const CopyBox& 
     sub_range(j, kSubElems, g.nr * g.nc, &lo, &hi);
     const E* S = reinterpret_cast<const E*>(k.src);
     E* D = reinterpret_cast<E*>(k.dst);
-    for (uint32_t i = lo + threadIdx.x; i < hi; i += kCopyThreads) {
+    for (uint32_t i = lo + threadIdx.x; i < hi; i += kSubThreads) {
       const uint32_t r = i / g.nc, c = i - r * g.nc;
       D[r * (k.dld / es) + c] = S[r * (k.sld / es) + c];
     }
@@ -112,7 +111,7 @@ __device__ __forceinline__ void copy_sub_kind(const CopyArgs& a, const CopyBox& 
 }
 
 template <bool kPack>
-__global__ __launch_bounds__(kCopyThreads) void copy_sub_kernel(CopyArgs a) {
+__global__ __launch_bounds__(kSubThreads) void copy_sub_kernel(CopyArgs a) {
   const uint32_t t = blockIdx.x / kSubPerTile, j = blockIdx.x % kSubPerTile;
   const uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
   const CopyBox b = a.boxes[bi];
@@ -275,9 +274,9 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
     const uint64_t nwg = uint64_t(ntiles) * kSubPerTile;
     if (nwg > uint64_t(INT32_MAX)) return hipErrorInvalidValue;
     if (pack)
-      hipLaunchKernelGGL((copy_sub_kernel<true>), dim3(uint32_t(nwg)), dim3(kCopyThreads), 0, stream, a);
+      hipLaunchKernelGGL((copy_sub_kernel<true>), dim3(uint32_t(nwg)), dim3(kSubThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL((copy_sub_kernel<false>), dim3(uint32_t(nwg)), dim3(kCopyThreads), 0, stream, a);
+      hipLaunchKernelGGL((copy_sub_kernel<false>), dim3(uint32_t(nwg)), dim3(kSubThreads), 0, stream, a);
     return hipGetLastError();
   }
   const uint32_t g = grid < ntiles ? grid : ntiles;

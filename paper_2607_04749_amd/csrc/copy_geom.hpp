@@ -59,14 +59,17 @@ __host__ __device__ inline uint64_t tile_msg_elem(const CopyBox& b, const TileGe
   return b.m_off + uint64_t(g.r0) * b.m_ld + g.c0;
 }
 
-// Sub-chunks of the all-kinds launch: one workgroup per sub-chunk j of tile t
-// (kSubPerTile per tile).  For each kind, sub-chunk j covers the tile's
-// vectors [j * kSubElems / vw, (j + 1) * kSubElems / vw) when the kind moves
-// in 16-byte vectors of vw elements, else its elements
+// Sub-chunks of the all-kinds launch: one workgroup of kSubThreads threads
+// (one wavefront) per sub-chunk j of tile t, kSubPerTile per tile.  For each
+// kind, sub-chunk j covers the tile's vectors [j * kSubElems / vw,
+// (j + 1) * kSubElems / vw) when the kind moves in 16-byte vectors of vw
+// elements (one vector per lane at most), else its elements
 // [j * kSubElems, (j + 1) * kSubElems), both in row-major order over the
 // tile and clipped to the tile's size.
-constexpr uint32_t kSubPerTile = 16;
-constexpr uint32_t kSubElems = kTileElems / kSubPerTile;  // 1024
+constexpr uint32_t kSubThreads = 64;
+constexpr uint32_t kSubPerTile = 64;
+constexpr uint32_t kSubElems = kTileElems / kSubPerTile;  // 256
+static_assert(kSubElems / 4 <= kSubThreads, "a 4-byte kind's sub-chunk must fit one vector per lane");
 
 // Whether the kind of element size es moves a tile in 16-byte vectors: the
 // box is vector-aligned for that size and every row of the tile is whole

@@ -86,7 +86,7 @@ static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned,
       const uint32_t unit = vk ? 16u / uint32_t(es) : 1u;  // elements per item
       const uint32_t per = kSubElems / unit;               // items per sub-chunk
       const uint32_t ipr = g.nc / unit;                    // items per row
-      if (vk && per > uint32_t(kCopyThreads)) FAIL("a vector sub-chunk needs more lanes than threads");
+      if (vk && per > kSubThreads) FAIL("a vector sub-chunk needs more lanes than threads");
       if (vk && g.nc % unit) FAIL("vector rows not whole vectors");
       std::vector<Iv> tw;
       for (uint32_t j = 0; j < kSubPerTile; ++j) {
