@@ -396,8 +396,8 @@ def main():
     achieved = (g_bytes / g_n) / ((g_ms / g_n) * 1e-3) / 1e9
     traffic = measured_traffic(w.name, side, g_bytes / g_n) if args.mode == "direct" and \
         not args.identity else None
-    # all four kinds run as copy_sub_kernel, one kind as the persistent copy_kernel
-    kernel = f"copy_sub_kernel ({side})" if kind is None else f"copy_kernel ({side}, kind {kind})"
+    # all four kinds run as copy_sub_kernel, one kind as copy_kind_kernel
+    kernel = f"copy_sub_kernel ({side})" if kind is None else f"copy_kind_kernel ({side}, kind {kind})"
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
     share = ("all ranks" if w.mode == "full" else
              f"pack of old rank {packers[0]}, unpack of new rank {unpackers[0]}")

@@ -89,19 +89,6 @@ int upload(etc_plan_t* P, int rank) {
     P->device = -1;
     return hip_fail(e, "hipGetDevice");
   }
-  int ncu = 0;
-  e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, P->device);
-  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  // copy engine launch shape: one resident workgroup per CU, enforced by
-  // reserving just over half of the CU's LDS per workgroup
-  int lds_cu = 0, lds_block = 0;
-  e = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, P->device);
-  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  e = hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, P->device);
-  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  P->copy_grid = uint32_t(std::max(1, ncu));
-  P->copy_lds_reserve = uint32_t(std::max(0, std::min(lds_block, lds_cu / 2 + 256)));
-
   std::vector<CopyBox> all;
   for (int s = 0; s < S; ++s) {
     if (rank != ETC_ALL_RANKS && my_src != s) continue;
@@ -483,9 +470,8 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
   void* peers[ETC_MAX_PEERS];
   for (size_t i = 0; i < t.peers.size(); ++i)  // the pack's peers are s's messages, in order
     peers[i] = static_cast<char*>(send_buf) + P->msgs[P->src_first[s] + i].displ;
-  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 0xFu, etc::kMsgSections, arenas, peers,
-                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, 0xFu, etc::kMsgSections,
+                                  arenas, peers, int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
   return ETC_OK;
 }
@@ -506,9 +492,8 @@ int etc_unpack(const etc_plan_t* P, int d, const void* const* msg, void* const d
     if (!aligned(p, 256)) return fail(ETC_ERR_ALIGN, "msg[" + std::to_string(t.peers[i]) + "] is not 256-byte aligned");
     peers[i] = const_cast<void*>(p);
   }
-  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 0xFu, etc::kMsgSections, dst_arena, peers,
-                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, 0xFu, etc::kMsgSections,
+                                  dst_arena, peers, int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
   return ETC_OK;
 }
@@ -552,9 +537,8 @@ int etc_pack_kind(const etc_plan_t* P, int s, int kind, const void* src_arena, v
   void* peers[ETC_MAX_PEERS];
   for (size_t j = 0; j < t.peers.size(); ++j)
     peers[j] = static_cast<char*>(chunk_buf) + P->msgs[P->src_first[s] + j].chunk_displ[i];
-  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 1u << kind, etc::kMsgOneKind, arenas, peers,
-                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(true, P->d_boxes + t.first, t.nbox, t.ntiles, 1u << kind, etc::kMsgOneKind,
+                                  arenas, peers, int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
   return ETC_OK;
 }
@@ -580,9 +564,8 @@ int etc_unpack_kind(const etc_plan_t* P, int d, int kind, const void* const* msg
   }
   void* arenas[4] = {nullptr, nullptr, nullptr, nullptr};
   arenas[kind] = dst_arena;
-  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 1u << kind, etc::kMsgOneKind, arenas, peers,
-                                  int(t.peers.size()), static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, 1u << kind, etc::kMsgOneKind,
+                                  arenas, peers, int(t.peers.size()), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
   return ETC_OK;
 }
@@ -599,9 +582,8 @@ int etc_refer(const etc_plan_t* P, int d, const void* const src_arena[4], void* 
   if ((rc = check_arenas(const_cast<const void* const*>(dst_arena), "dst_arena"))) return rc;
   void* sources[4];
   for (int k = 0; k < 4; ++k) sources[k] = const_cast<void*>(src_arena[k]);
-  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 0xFu, etc::kMsgArenas, dst_arena, sources, 4,
-                                  static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, 0xFu, etc::kMsgArenas,
+                                  dst_arena, sources, 4, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "refer launch");
   return ETC_OK;
 }
@@ -622,9 +604,8 @@ int etc_refer_kind(const etc_plan_t* P, int d, int kind, const void* src_arena, 
   void* sources[4] = {nullptr, nullptr, nullptr, nullptr};
   arenas[kind] = dst_arena;
   sources[kind] = const_cast<void*>(src_arena);
-  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, P->copy_grid,
-                                  P->copy_lds_reserve, 1u << kind, etc::kMsgArenas, arenas, sources, 4,
-                                  static_cast<hipStream_t>(stream));
+  hipError_t e = etc::launch_copy(false, P->d_boxes + t.first, t.nbox, t.ntiles, 1u << kind, etc::kMsgArenas,
+                                  arenas, sources, 4, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "refer launch");
   return ETC_OK;
 }

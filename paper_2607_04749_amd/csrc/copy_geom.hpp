@@ -12,16 +12,6 @@
 
 namespace etc {
 
-constexpr uint32_t kXcds = 8;  // MI355X: 8 accelerator complex dies, 32 CUs each
-
-// First tile of workgroup `block` in a grid of `grid` workgroups; later ones
-// follow every `grid` tiles.  Workgroups are dispatched round-robin over the
-// XCDs, so block mod 8 is its XCD; within each round of `grid` tiles the
-// workgroups of one XCD take a contiguous run of grid / 8 tiles.
-__host__ __device__ inline uint32_t first_tile(uint32_t block, uint32_t grid) {
-  return grid % kXcds == 0 ? (block % kXcds) * (grid / kXcds) + block / kXcds : block;
-}
-
 // Index of the box holding tile t: the last box with tile0 <= t.
 __host__ __device__ inline uint32_t box_of_tile(const CopyBox* boxes, uint32_t nbox, uint32_t t) {
   uint32_t lo = 0, hi = nbox;
@@ -59,16 +49,21 @@ __host__ __device__ inline uint64_t tile_msg_elem(const CopyBox& b, const TileGe
   return b.m_off + uint64_t(g.r0) * b.m_ld + g.c0;
 }
 
-// Sub-chunks of the all-kinds launch: one workgroup of kSubThreads threads
-// (one wavefront) per sub-chunk j of tile t, kSubPerTile per tile.  For each
+// Sub-chunks: a tile splits into kSubPerTile sub-chunks, copied by
+// workgroups of kSubThreads threads (one wavefront); a launch of all four
+// kinds gives workgroup kSubPerTile * t + j sub-chunk j of tile t.  For each
 // kind, sub-chunk j covers the tile's vectors [j * kSubElems / vw,
 // (j + 1) * kSubElems / vw) when the kind moves in 16-byte vectors of vw
 // elements (one vector per lane at most), else its elements
 // [j * kSubElems, (j + 1) * kSubElems), both in row-major order over the
 // tile and clipped to the tile's size.
+// A launch of one kind gives each workgroup kKindGroup consecutive
+// sub-chunks of one tile instead.
 constexpr uint32_t kSubThreads = 64;
 constexpr uint32_t kSubPerTile = 64;
 constexpr uint32_t kSubElems = kTileElems / kSubPerTile;  // 256
+constexpr uint32_t kKindGroup = 8;
+static_assert(kSubPerTile % kKindGroup == 0, "whole groups per tile");
 static_assert(kSubElems / 4 <= kSubThreads, "a 4-byte kind's sub-chunk must fit one vector per lane");
 
 // Whether the kind of element size es moves a tile in 16-byte vectors: the

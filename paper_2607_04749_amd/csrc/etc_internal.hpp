@@ -100,7 +100,6 @@ struct CopyTable {
 };
 
 constexpr uint32_t kTileElems = 16384;  // nominal tile: 16384 elements per kind
-constexpr int kCopyThreads = 256;
 constexpr int kCmThreads = 256;
 
 // What the message side of a copy launch is.
@@ -111,13 +110,11 @@ enum MsgMode : uint32_t {
 };
 
 // kernel launchers (copy.hip, cost.hip)
-// kind_mask: kinds to copy (bit k): all four (one workgroup per tile
-// sub-chunk; grid and lds_reserve unused) or one (persistent grid of `grid`
-// workgroups, each reserving lds_reserve bytes of LDS); any other mask is
-// hipErrorInvalidValue
-hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles,
-                       uint32_t grid, uint32_t lds_reserve, uint32_t kind_mask, MsgMode mode,
-                       void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
+// kind_mask: kinds to copy (bit k): all four (one sub-chunk of each kind per
+// workgroup) or one (kKindGroup sub-chunks per workgroup); any other mask is
+// hipErrorInvalidValue, and so is a grid over 2^31 - 1 workgroups
+hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles, uint32_t kind_mask,
+                       MsgMode mode, void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
 // Routing context of a plan: both grids and the failed source ranks (bitmap,
 // nullptr when none).  Device copies point at device memory.
 struct RouteCtx {
@@ -187,8 +184,6 @@ struct etc_plan_s {
 
   // device side
   int device = -1;
-  uint32_t copy_grid = 0;       // one-kind copy launches: persistent grid, one workgroup per CU
-  uint32_t copy_lds_reserve = 0;  // dynamic LDS per one-kind copy workgroup (occupancy cap)
   etc::RouteTensor* d_route_tensors = nullptr;
   int32_t* d_home = nullptr;  // device copy of home (D entries)
   uint32_t* d_failed = nullptr;  // device copy of failed_bits

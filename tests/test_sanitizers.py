@@ -68,12 +68,12 @@ def test_tile_walk_under_sanitizers(binaries):
         if w.name in ("llama-70b", "llama-13b"):
             continue  # the largest plans are covered without sanitizers; keep this test short
         for refer in (False, True):
-            jobs.append(tw._args(w.model, w.src, w.dst, 256, refer, "sketch"))
+            jobs.append(tw._args(w.model, w.src, w.dst, refer, "sketch"))
     for m in MICRO_MODELS.values():
         for a, b in cfg_pairs(m)[::7]:
-            jobs.append(tw._args(m, a, b, 7, True, "identity"))
+            jobs.append(tw._args(m, a, b, True, "identity"))
     for m, a, b in cases(16, base=0x5A17):
-        jobs.append(tw._args(m, a, b, 256, True, "sketch"))
+        jobs.append(tw._args(m, a, b, True, "sketch"))
 
     def one(args):
         return args, subprocess.run([binaries["tilewalk"], *args], capture_output=True, text=True,

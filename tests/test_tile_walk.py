@@ -1,7 +1,7 @@
 """The copy tables on the host, no GPU: tests/tilewalk/tilewalk.cpp replays the
-copy kernel's tile walk over every launch the planner builds (pack, unpack,
-Refer; all kinds and one kind at a time; the device's grid and a small odd
-one) and checks bounds, alignment and exact write coverage.  Plans: the five
+copy kernels' sub-chunk walk over every launch the planner builds (pack,
+unpack, Refer; all kinds and one kind at a time) and checks bounds,
+alignment and exact write coverage.  Plans: the five
 workloads, micro models, data parallelism with failed ranks, coalesced and
 random configurations, under the identity pairing, the sketch and direct
 Refer.  This is the check run on the CPU before a plan shape first runs on
@@ -48,11 +48,11 @@ def tilewalk():
     return _binary()
 
 
-def _args(model, a, b, grid, refer, pairing, failed=()):
+def _args(model, a, b, refer, pairing, failed=()):
     if not isinstance(pairing, str):
         pairing = ",".join(str(int(x)) for x in pairing)
     return [*map(str, model.astuple()), str(a.tp), str(a.pp), str(a.dp), str(b.tp), str(b.pp),
-            str(b.dp), str(grid), "1" if refer else "0", pairing, *map(str, failed)]
+            str(b.dp), "1" if refer else "0", pairing, *map(str, failed)]
 
 
 def _run_all(exe, jobs):
@@ -79,8 +79,8 @@ def test_workloads(tilewalk):
     for w in WORKLOADS.values():
         for refer in (False, True):
             for pairing in ("identity", "sketch"):
-                jobs.append(_args(w.model, w.src, w.dst, 256, refer, pairing))
-        jobs.append(_args(w.model, w.dst, w.src, 256, False, "sketch"))
+                jobs.append(_args(w.model, w.src, w.dst, refer, pairing))
+        jobs.append(_args(w.model, w.dst, w.src, False, "sketch"))
     assert _run_all(tilewalk, jobs) == 25
 
 
@@ -89,8 +89,8 @@ def test_micro_models(tilewalk):
     for m in MICRO_MODELS.values():
         for a, b in cfg_pairs(m)[::3]:
             for refer in (False, True):
-                jobs.append(_args(m, a, b, 256, refer, "identity"))
-                jobs.append(_args(m, a, b, 7, refer, _oracle_sketch(m, a, b)))
+                jobs.append(_args(m, a, b, refer, "identity"))
+                jobs.append(_args(m, a, b, refer, _oracle_sketch(m, a, b)))
     assert _run_all(tilewalk, jobs) > 100
 
 
@@ -100,8 +100,8 @@ def test_data_parallel_and_failures(tilewalk):
     for a, b, failed in ((P(2, 1, 2), P(1, 2, 3), ()), (P(2, 1, 3), P(1, 2, 2), (1, 2)),
                          (P(2, 2, 2), P(4, 1, 1), (0, 5)), (P(1, 2, 3), P(1, 2, 1), (2,))):
         for refer in (False, True):
-            jobs.append(_args(m, a, b, 256, refer, "identity", failed))
-            jobs.append(_args(m, a, b, 256, refer, _oracle_sketch(m, a, b, list(failed)), failed))
+            jobs.append(_args(m, a, b, refer, "identity", failed))
+            jobs.append(_args(m, a, b, refer, _oracle_sketch(m, a, b, list(failed)), failed))
     _run_all(tilewalk, jobs)
 
 
@@ -114,15 +114,15 @@ def test_coalesced_pairings(tilewalk):
             pl, _ = oracle.defrag(a.world, b.world, sk, mode=mode)
             co = np.where(pl < a.world, pl, -1)
             for refer in (False, True):
-                jobs.append(_args(m, a, b, 256, refer, co))
+                jobs.append(_args(m, a, b, refer, co))
     _run_all(tilewalk, jobs)
 
 
 def test_random_configurations(tilewalk):
     jobs = []
     for m, a, b in cases(48):
-        jobs.append(_args(m, a, b, 256, False, "identity"))
-        jobs.append(_args(m, a, b, 256, True, _oracle_sketch(m, a, b)))
+        jobs.append(_args(m, a, b, False, "identity"))
+        jobs.append(_args(m, a, b, True, _oracle_sketch(m, a, b)))
     _run_all(tilewalk, jobs)
 
 
@@ -134,7 +134,6 @@ def test_contiguous_run_beyond_2_32_elements(tilewalk):
     m = ModelShape(GPT, 2, 17, 1, 1, 8, 2 ** 28 + 1, 0, 1)
     jobs = []
     for b in (P(1, 1), P(1, 2)):
-        for grid in (256, 7):
-            for refer in (False, True):
-                jobs.append(_args(m, P(1, 1), b, grid, refer, "identity"))
+        for refer in (False, True):
+            jobs.append(_args(m, P(1, 1), b, refer, "identity"))
     _run_all(tilewalk, jobs)

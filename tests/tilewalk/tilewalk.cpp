@@ -1,7 +1,7 @@
 // tilewalk.cpp -- host replay of the copy kernels' walks over the copy
 // tables the planner builds (pack, unpack and Refer; all kinds at once, one
-// workgroup per sub-chunk of a tile; one kind at a time, a persistent grid of
-// any size).  For every tile it checks that each row stays inside its arena,
+// sub-chunk of each kind per workgroup; one kind at a time, kKindGroup
+// sub-chunks per workgroup).  For every tile it checks that each row stays inside its arena,
 // message section or source arena, that vector accesses are 16-byte aligned,
 // that a sub-chunk needs no more lanes than a workgroup has, and that the
 // writes of a launch cover the target bytes exactly once: each message
@@ -12,7 +12,7 @@
 // header; it computes no expected values.
 //
 // usage: tilewalk arch L h nh nkv ffn V max_pos tied flags  tp pp dp  tp pp dp
-//                 grid refer pairing [failed ...]
+//                 refer pairing [failed ...]
 //   refer: 1 builds the plan with ETC_PLAN_DIRECT_REFER
 //   pairing: "identity", "sketch", or comma-separated pair[d] (-1 = none)
 #include <algorithm>
@@ -59,13 +59,17 @@ static std::vector<Iv> merge_tile(std::vector<Iv> w, const char* what) {
   return m;
 }
 
-// Replay an all-kinds launch as the sub-chunk kernel runs it: workgroup
-// t * kSubPerTile + j copies sub-chunk j of every kind of tile t.
-static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint64_t arena_elems,
-                       const std::vector<uint64_t>& peer_bytes, std::vector<std::vector<Iv>> W[4],
-                       std::vector<Iv> A[4], bool arenas) {
+// Replay a launch as the kernels run it: for all four kinds, workgroup
+// t * kSubPerTile + j copies sub-chunk j of every kind of tile t; for one
+// kind, workgroup t * (kSubPerTile / kKindGroup) + q copies its sub-chunks
+// [q * kKindGroup, (q + 1) * kKindGroup) of tile t.  Either way every
+// sub-chunk j of every tile is copied once per kind in the launch.
+static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask,
+                       uint64_t arena_elems, const std::vector<uint64_t>& peer_bytes,
+                       std::vector<std::vector<Iv>> W[4], std::vector<Iv> A[4], bool arenas) {
   const uint32_t nbox = uint32_t(v.size() - 1), ntiles = v.back().tile0;
-  if (uint64_t(ntiles) * kSubPerTile > uint64_t(INT32_MAX)) { FAIL("grid over 2^31 - 1 workgroups"); return; }
+  const uint32_t per_tile = kind_mask == 0xFu ? kSubPerTile : kSubPerTile / kKindGroup;
+  if (uint64_t(ntiles) * per_tile > uint64_t(INT32_MAX)) { FAIL("grid over 2^31 - 1 workgroups"); return; }
   for (uint32_t t = 0; t < ntiles; ++t) {
     const uint32_t bi = box_of_tile(v.data(), nbox, t);  // the same for every j of the tile
     if (bi >= nbox) { FAIL("tile past last box"); return; }
@@ -74,6 +78,7 @@ static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned,
     if (g.nr == 0 || g.nc == 0 || g.r0 >= b.rows || g.c0 >= b.cols) FAIL("empty/outside tile");
     if (!arenas && b.peer >= peer_bytes.size()) { FAIL("peer slot %u out of range", b.peer); return; }
     for (int k = 0; k < 4; ++k) {
+      if (!(kind_mask & (1u << k))) continue;
       const int es = k == 0 ? 2 : 4;
       const uint64_t ae = tile_arena_elem(b, g), me = tile_msg_elem(b, g);
       const uint64_t sec = (sectioned && !arenas) ? section_byte(b.msg_npad, k) : 0;
@@ -115,59 +120,20 @@ static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned,
   }
 }
 
-// Replay one launch exactly as the kernel walks it.  peer_bytes[p] = length of
-// peer p's message; W[k][p] collects message writes (pack), A[k] arena writes.
-static void replay(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask, uint32_t G,
+// Replay one launch.  peer_bytes[p] = length of peer p's message; W[k][p]
+// collects message writes (pack), A[k] arena writes.
+static void replay(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask,
                    uint64_t arena_elems, const std::vector<uint64_t>& peer_bytes,
                    std::vector<std::vector<Iv>> W[4], std::vector<Iv> A[4], bool arenas = false) {
-  const uint32_t nbox = uint32_t(v.size() - 1), ntiles = v.back().tile0;
-  if (ntiles == 0) return;
-  if (kind_mask == 0xFu) {
-    replay_sub(v, pack, sectioned, arena_elems, peer_bytes, W, A, arenas);
+  if (v.back().tile0 == 0) return;
+  if (kind_mask != 0xFu && (kind_mask == 0 || (kind_mask & (kind_mask - 1)))) {
+    FAIL("a launch of more than one kind but not all four");
     return;
   }
-  if (kind_mask & (kind_mask - 1)) { FAIL("a launch of more than one kind but not all four"); return; }
-  G = G < ntiles ? G : ntiles;
-  for (uint32_t bid = 0; bid < G; ++bid) {
-    uint32_t t = first_tile(bid, G);
-    uint32_t bi = box_of_tile(v.data(), nbox, t);
-    CopyBox b = v[bi]; uint32_t next0 = v[bi + 1].tile0;
-    for (; t < ntiles; t += G) {
-      while (t >= next0) { ++bi; if (bi >= nbox) { FAIL("walked past last box"); return; } b = v[bi]; next0 = v[bi + 1].tile0; }
-      TileGeom g = tile_geom(b, t, next0);
-      if (g.nr == 0 || g.nc == 0 || g.r0 >= b.rows || g.c0 >= b.cols) FAIL("empty/outside tile");
-      if (!arenas && b.peer >= peer_bytes.size()) { FAIL("peer slot %u out of range", b.peer); return; }
-      for (int k = 0; k < 4; ++k) {
-        if (!(kind_mask & (1u << k))) continue;
-        const int es = k == 0 ? 2 : 4;
-        const uint64_t ae = tile_arena_elem(b, g), me = tile_msg_elem(b, g);
-        const uint64_t sec = (sectioned && !arenas) ? section_byte(b.msg_npad, k) : 0;
-        const uint64_t sec_end = arenas ? peer_bytes[k] : sec + b.msg_npad * es;
-        const bool vec = (b.vec >> (es == 2 ? 0 : 1)) & 1;
-        const uint64_t sp = (pack ? uint64_t(b.a_ld) : b.m_ld) * es, dp = (pack ? b.m_ld : uint64_t(b.a_ld)) * es;
-        if (!arenas && b.m_ld != b.cols) FAIL("message box with a row stride");
-        if (std::max(sp, dp) * (g.nr - 1) + uint64_t(g.nc) * es >= (1ull << 31)) FAIL("tile extent over 2^31");
-        for (uint32_t r = 0; r < g.nr; ++r) {
-          const uint64_t alo = (ae + uint64_t(r) * b.a_ld) * es, ahi = alo + uint64_t(g.nc) * es;
-          const uint64_t mlo = sec + (me + uint64_t(r) * b.m_ld) * es, mhi = mlo + uint64_t(g.nc) * es;
-          if (ahi > arena_elems * es) FAIL("arena OOB kind %d", k);
-          if ((!arenas && mhi > peer_bytes[b.peer]) || mhi > sec_end) FAIL("message OOB peer %u kind %d", b.peer, k);
-          if (arenas && (b.pad || b.msg_npad)) FAIL("refer box with padding");
-          if (vec && (alo % 16 || mlo % 16)) FAIL("vector misaligned kind %d", k);
-          if (vec && g.nr > 1 && (uint64_t(g.nc) * es) % 16) FAIL("2-D vector rows not whole vectors");
-          if (pack) W[k][b.peer].push_back({mlo, mhi}); else A[k].push_back({alo, ahi});
-        }
-        if (pack && g.last && b.pad) {
-          const uint64_t plo = sec + (b.m_off + uint64_t(b.rows) * b.cols) * es, phi = plo + uint64_t(b.pad) * es;
-          if (phi > sec_end) FAIL("pad overrun");
-          W[k][b.peer].push_back({plo, phi});
-        }
-      }
-    }
-  }
+  replay_sub(v, pack, sectioned, kind_mask, arena_elems, peer_bytes, W, A, arenas);
 }
 
-static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
+static void check_plan(etc_plan_t& P, const char* name) {
   const int S = P.src.world(), D = P.dst.world();
   for (int sectioned = 1; sectioned >= 0; --sectioned) {
     for (int s = 0; s < S; ++s) {
@@ -180,7 +146,7 @@ static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
         for (int d : peers) pb.push_back(npad_of(P, s, d) * (sectioned ? 14 : (k ? 4 : 2)));
         std::vector<std::vector<Iv>> W[4]; std::vector<Iv> A[4];
         for (int kk = 0; kk < 4; ++kk) W[kk].assign(peers.size(), {});
-        replay(v, true, sectioned, mask, grid, P.src_lay(s).elems, pb, W, A);
+        replay(v, true, sectioned, mask, P.src_lay(s).elems, pb, W, A);
         for (int kk = 0; kk < 4; ++kk) {
           if (!(mask & (1u << kk))) continue;
           const int es = kk ? 4 : 2;
@@ -201,7 +167,7 @@ static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
         std::vector<uint64_t> pb;
         for (int s : peers) pb.push_back(npad_of(P, s, d) * (sectioned ? 14 : (k ? 4 : 2)));
         std::vector<std::vector<Iv>> W[4]; std::vector<Iv> A[4];
-        replay(v, false, sectioned, mask, grid, P.dst_lay(d).elems, pb, W, A);
+        replay(v, false, sectioned, mask, P.dst_lay(d).elems, pb, W, A);
         if (P.flags & ETC_PLAN_DIRECT_REFER) {  // Refer writes complete the target
           uint64_t rb = 0;
           auto rv = build_refer_boxes(P, d, &rb);
@@ -211,7 +177,7 @@ static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
             const uint64_t se = P.src_lay(h).elems;
             std::vector<uint64_t> sb = {se * 2, se * 4, se * 4, se * 4};
             std::vector<std::vector<Iv>> RW[4];
-            replay(rv, false, false, mask, grid, P.dst_lay(d).elems, sb, RW, A, true);
+            replay(rv, false, false, mask, P.dst_lay(d).elems, sb, RW, A, true);
           }
         }
         for (int kk = 0; kk < 4; ++kk) {
@@ -228,8 +194,8 @@ static void check_plan(etc_plan_t& P, const char* name, uint32_t grid) {
 
 
 int main(int argc, char** argv) {
-  if (argc < 20) {
-    fprintf(stderr, "usage: tilewalk arch L h nh nkv ffn V max_pos tied flags tp pp dp tp pp dp grid refer pairing [failed...]\n");
+  if (argc < 19) {
+    fprintf(stderr, "usage: tilewalk arch L h nh nkv ffn V max_pos tied flags tp pp dp tp pp dp refer pairing [failed...]\n");
     return 2;
   }
   etc_model_desc m{};
@@ -241,7 +207,6 @@ int main(int argc, char** argv) {
   etc_parallel_cfg a{atoi(argv[i]), atoi(argv[i + 1]), atoi(argv[i + 2])};
   etc_parallel_cfg b{atoi(argv[i + 3]), atoi(argv[i + 4]), atoi(argv[i + 5])};
   i += 6;
-  const uint32_t grid = uint32_t(atoi(argv[i++]));
   const bool refer = atoi(argv[i++]) != 0;
   const std::string pairing = argv[i++];
   etc_plan_t P;
@@ -278,7 +243,7 @@ int main(int argc, char** argv) {
       }
     }
     build_host_plan(P);
-    check_plan(P, "plan", grid);
+    check_plan(P, "plan");
   } catch (PlanError& e) {
     fprintf(stderr, "plan error %d %s\n", e.code, e.what());
     return 1;
