@@ -94,7 +94,25 @@ static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned,
       if (vk && per > kSubThreads) FAIL("a vector sub-chunk needs more lanes than threads");
       if (vk && g.nc % unit) FAIL("vector rows not whole vectors");
       std::vector<Iv> tw;
-      for (uint32_t j = 0; j < kSubPerTile; ++j) {
+      // the sub-chunks of tile t, in the order and with the index arithmetic
+      // of the kernels' workgroups
+      std::vector<uint32_t> subs;
+      for (uint32_t w = t * per_tile; w < (t + 1) * per_tile; ++w) {
+        if (kind_mask == 0xFu) {
+          if (w / kSubPerTile != t) FAIL("workgroup %u maps to another tile", w);
+          subs.push_back(w % kSubPerTile);
+        } else {
+          constexpr uint32_t groups = kSubPerTile / kKindGroup;
+          if (w / groups != t) FAIL("workgroup %u maps to another tile", w);
+          for (uint32_t i = 0; i < kKindGroup; ++i) subs.push_back((w % groups) * kKindGroup + i);
+        }
+      }
+      std::vector<char> seen(kSubPerTile, 0);
+      for (uint32_t j : subs) {
+        if (j >= kSubPerTile || seen[j]++) FAIL("sub-chunk %u of tile %u copied twice or out of range", j, t);
+      }
+      for (uint32_t j : subs) {
+        if (j >= kSubPerTile) continue;
         uint32_t lo, hi;
         sub_range(j, per, g.nr * ipr, &lo, &hi);
         for (uint32_t r = lo / (ipr ? ipr : 1); lo < hi && r <= (hi - 1) / ipr; ++r) {
