@@ -223,12 +223,14 @@ typedef struct {
  * ETC_PLAN_HOST_ONLY no device memory is touched.
  * A routed run of contiguous elements may exceed 2^32 elements (it is copied
  * in pieces of 2^31); no tensor size limit applies beyond the int32 fields of
- * etc_model_desc.
+ * etc_model_desc and the workgroup limit below.
  * On success *out owns host and device memory until etc_plan_free.
  * Errors: INVALID_ARG (also a bad pairing or failed list), INDIVISIBLE,
  * UNSUPPORTED (GPT with GQA, more than 65536 ranks, a rank exchanging messages
- * with more than ETC_MAX_PEERS peers), UNRECOVERABLE (every replica of some
- * needed data failed), RANK, NOMEM, HIP. */
+ * with more than ETC_MAX_PEERS peers; with device tables, a rank's copy that
+ * needs more than 2^31 - 1 GPU workgroups, i.e. about 5.5e11 routed
+ * elements), UNRECOVERABLE (every replica of some needed data failed), RANK,
+ * NOMEM, HIP. */
 ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
                      const etc_parallel_cfg* dst, const etc_plan_options* opt, etc_plan_t** out);
 

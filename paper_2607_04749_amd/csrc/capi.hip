@@ -8,6 +8,7 @@
 #include <new>
 #include <string>
 
+#include "copy_geom.hpp"
 #include "etc.h"
 #include "etc_internal.hpp"
 #include "plan.hpp"
@@ -120,6 +121,11 @@ int upload(etc_plan_t* P, int rank) {
     t.built = true;
     all.insert(all.end(), v.begin(), v.end());
   }
+  // the copy kernels launch one workgroup per sub-chunk of every tile
+  for (const auto* tabs : {&P->pack_tab, &P->unpack_tab, &P->refer_tab})
+    for (const CopyTable& t : *tabs)
+      if (uint64_t(t.ntiles) * kSubPerTile > uint64_t(INT32_MAX))
+        return fail(ETC_ERR_UNSUPPORTED, "a rank's copy needs more than 2^31 - 1 GPU workgroups");
   if (!all.empty()) {
     e = hipMalloc(&P->d_boxes, all.size() * sizeof(CopyBox));
     if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));

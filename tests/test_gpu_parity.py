@@ -156,6 +156,22 @@ def test_error_paths_on_device():
     torch.cuda.synchronize()
 
 
+def test_copy_grid_limit():
+    """A rank whose copy would need more than 2^31 - 1 workgroups is refused
+    when the device tables are built, before any allocation: GPT with hidden
+    1024 and vocab 2^30, one rank, so the embedding alone is 2^40 elements
+    (2^26 tiles of 64 sub-chunks).  The host-only plan of the same shape is
+    fine."""
+    from paper_2607_04749_amd.workloads import GPT, ModelShape
+    m = ModelShape(GPT, 2, 1024, 1, 1, 8, 2 ** 30, 0, 1)
+    say("copy grid limit: GPT hidden 1024, vocab 2^30, TP1")
+    host = etc.etc_plan(m, Parallel(1, 1), Parallel(1, 1), flags=etc.PLAN_HOST_ONLY)
+    assert host.send_layout(0)[0][0] == 14 * (2 ** 40 + 2 * (1024 * 1024 * 4 + 8 * 1024 * 2 + 1024 * 9 + 8) + 2 * 1024)
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan(m, Parallel(1, 1), Parallel(1, 1))
+    assert e.value.code == etc.ERR_UNSUPPORTED
+
+
 def test_empty_launches():
     """Identity configuration with direct Refer: every message is empty, so
     each pack and unpack (all kinds, or one) has nothing to copy.  They return
