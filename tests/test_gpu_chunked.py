@@ -123,19 +123,22 @@ def test_micro_chunked_equals_full(name):
         _compare_with_oracle(m, a, b, 31)
 
 
-def test_llama_70b_share_chunked():
-    """The 70B share kind by kind at real shape, in the launch configuration
-    the chunked benchmark times (the oracle's sketch pairing, which the
-    library's sketch also finds): the whole target against the seeded values,
-    and sampled chunk message elements against the oracle's serialization."""
-    w = WORKLOADS["llama-70b"]
+@pytest.mark.parametrize("wl", ["llama-70b", "llama-7b", "llama-13b"])
+def test_share_chunked(wl):
+    """A share kind by kind at real shape, in the launch configuration the
+    chunked benchmark times (the oracle's sketch pairing, which the library's
+    sketch also finds): the whole target against the seeded values, and
+    sampled chunk message elements against the oracle's serialization.  70B
+    is contiguous throughout; the 7B unpack and the 13B pack copy strided
+    rows."""
+    w = WORKLOADS[wl]
     pr = oracle.sketch(oracle.matrices(w.model, w.src, w.dst)["cost"])[0]
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr)
     s0, d0 = plan.process(w.pack_rank)
     feeders = sorted({int(s) for s in np.nonzero(plan.recv_counts(d0))[0]} | {s0})
-    say("llama-70b chunked share: pack", s0, "unpack", d0, "sources", feeders)
+    say(wl, "chunked share: pack", s0, "unpack", d0, "sources", feeders)
     src = seeded_arenas(w.model, w.src, feeders, w.seed)
-    rng = np.random.default_rng(70)
+    rng = np.random.default_rng(sum(map(ord, wl)))
     dst = [None] * 4
     for k in range(4):
         bufs = {}
