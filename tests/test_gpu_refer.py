@@ -55,15 +55,19 @@ def test_random_direct_refer(i):
     full_compare(m, a, b, 0xEF + i, pair=_sketch(m, a, b), round_trip=False, direct_refer=True)
 
 
-def test_llama_70b_share_direct_refer():
-    """Process 0 keeps half of its new rank's state (its own layers) and
-    receives the other half from one peer: refer + unpack at real shape."""
-    w = WORKLOADS["llama-70b"]
+@pytest.mark.parametrize("wl", ["llama-70b", "llama-7b", "llama-13b"])
+def test_share_direct_refer(wl):
+    """Process 0's share with direct Refer at real shape.  70B: the new rank
+    keeps half of its state (its own layers) and receives the other half
+    from one peer.  7B: it keeps its old shard, strided on both sides, and
+    receives the rest from one peer.  13B: everything it needs is kept, so
+    the unpack has nothing to do."""
+    w = WORKLOADS[wl]
     pr = _sketch(w.model, w.src, w.dst)
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr, flags=etc.PLAN_DIRECT_REFER)
     s0, d0 = plan.process(w.pack_rank)
     feeders = sorted(int(s) for s in np.nonzero(plan.recv_counts(d0))[0])
-    say("llama-70b direct refer: process", w.pack_rank, "old", s0, "new", d0, "feeders", feeders,
+    say(wl, "direct refer: process", w.pack_rank, "old", s0, "new", d0, "feeders", feeders,
         "refer GB", plan.refer_bytes(d0) / 1e9)
     assert s0 not in feeders and plan.refer_bytes(d0) > 0
     src = seeded_arenas(w.model, w.src, sorted(set(feeders) | {s0}), w.seed)
