@@ -11,6 +11,11 @@ and the new rank it becomes.
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
                     [--identity] [--mode direct|chunked|coalesced|refer]
 
+With no --workload the run times the Llama-70B share (the line's value and
+roofline) and then, after freeing its buffers, the Llama-7B share, reported
+under "shares" with its own rate, roofline and CPU baseline: the two shares
+the 70 % target is stated on.  --workload NAME times that workload alone.
+
 Modes: direct (default) packs and unpacks all four state kinds in one launch
 each; chunked moves one state kind at a time through per-kind chunk buffers
 (state chunking, Sec. III-D), four pack and four unpack launches per step;
@@ -30,6 +35,7 @@ and on up to 16 threads (reported).
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -158,7 +164,8 @@ def cpu_baseline(w, pairing, layers=4, direct_refer=False):
             runs.append(time.perf_counter() - t0)
     dtn = sorted(runs)[1]
     return {"value": round(alg / dtn / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"tensors of layers {held[0]}-{held[-1]} ({len(sample)} tensors): pack of source {s0} + "
+            "sample": f"a {len(held)}-layer sample of the share, not the whole share: the tensors of layers "
+                      f"{held[0]}-{held[-1]} ({len(sample)} tensors), pack of source {s0} + "
                       f"unpack of target {d0}, {pairing} pairing, {alg / 1e9:.3f} GB algorithmic; "
                       f"{dtn:.2f} s on {threads} threads (one tensor per task, median of 3), {dt1:.2f} s "
                       f"({alg / dt1 / 1e9:.3f} GB/s) on one thread; host {host_cpu()}"}
@@ -186,33 +193,29 @@ def host_cpu():
     return f"{name} ({host_threads()} logical CPUs available)"
 
 
-def main():
+def parse_args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama-70b")
+    ap.add_argument("--workload", default=None,
+                    help="one workload alone (default: the 70B share, then the 7B share)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--identity", action="store_true", help="identity pairing instead of the sketch")
     ap.add_argument("--mode", choices=("direct", "chunked", "coalesced", "refer"), default="direct")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU's share of the migration; multi-GPU runs are not "
-              "supported (--gpus must be 1)", file=sys.stderr)
-        sys.exit(2)
-    if args.identity and args.mode == "coalesced":
-        print("--identity and --mode coalesced exclude each other", file=sys.stderr)
-        sys.exit(2)
+    return ap.parse_args()
 
+
+def run_share(w, args):
+    """Time one workload's step; returns the fields of its bench line
+    (without cpu_baseline).  Every buffer it allocates is freed on return."""
     import numpy as np
     import torch
 
     import synth
     from paper_2607_04749_amd import etc
-    from paper_2607_04749_amd.workloads import ESIZE, WORKLOADS
+    from paper_2607_04749_amd.workloads import ESIZE
 
-    w = WORKLOADS[args.workload]
-    torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     pairing = "identity" if args.identity else ("coalesced" if args.mode == "coalesced" else "sketch")
@@ -430,10 +433,53 @@ def main():
         out["refer_GBps"] = rate(refer_bytes, refer_ms)
         out["refer_ms"] = round(refer_ms, 4)
         out["refer_bytes"] = refer_bytes
-    if not args.no_cpu_baseline:
-        log("cpu baseline (oracle, one thread) ...")
-        out["cpu_baseline"] = cpu_baseline(w, pairing, direct_refer=args.mode == "refer")
-    print(json.dumps(out), flush=True)
+    log(f"{w.name}: {value:.1f} GB/s ({value / PEAK_HBM_GBPS:.4f} of peak), {ms_per_step:.3f} ms per step")
+    return out, pairing
+
+
+SHARE_KEYS = ("value", "unit", "ms_per_step", "frac_of_peak", "pack_GBps", "unpack_GBps", "pack_ms",
+              "unpack_ms", "pack_bytes", "unpack_bytes", "launches_per_step", "cost_matrix_us",
+              "cost_matrix_cells", "sketch_us", "pairing", "d2d_copy_GBps", "plan_ms", "roofline",
+              "refer_GBps", "refer_ms", "refer_bytes")
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU's share of the migration; multi-GPU runs are not "
+              "supported (--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+    if args.identity and args.mode == "coalesced":
+        print("--identity and --mode coalesced exclude each other", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_04749_amd.workloads import WORKLOADS
+
+    torch.cuda.set_device(0)
+    names = [args.workload] if args.workload else ["llama-70b", "llama-7b"]
+    line, shares = None, {}
+    for name in names:
+        w = WORKLOADS[name]
+        out, pairing = run_share(w, args)
+        gc.collect()  # the share's buffers go before the next share allocates its own
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        if not args.no_cpu_baseline:
+            log(f"{name}: cpu baseline (oracle) ...")
+            out["cpu_baseline"] = cpu_baseline(w, pairing, direct_refer=args.mode == "refer")
+        if line is None:
+            line = out
+        else:
+            shares[name] = {"workload": out["config"]["workload"],
+                            "alg_bytes_per_step": out["config"]["alg_bytes_per_step"],
+                            **{k: out[k] for k in SHARE_KEYS + ("cpu_baseline",) if k in out}}
+    if shares:
+        line["shares"] = shares
+    print(json.dumps(line), flush=True)
+
+
 
 
 if __name__ == "__main__":

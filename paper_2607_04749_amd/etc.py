@@ -146,6 +146,29 @@ def _ptr(x):
     return x.data_ptr()
 
 
+def _buf(x, need, what):
+    """Pointer of a device buffer that must hold at least `need` bytes.  A
+    tensor must be a contiguous GPU tensor of that many bytes, else
+    ValueError (the kernels would write past it); an integer pointer or None
+    is passed through as given."""
+    if x is None or isinstance(x, int):
+        return x
+    if not x.is_cuda or not x.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous GPU tensor")
+    n = x.numel() * x.element_size()
+    if n < need:
+        raise ValueError(f"{what} holds {n} bytes; the plan needs {need}")
+    return x.data_ptr()
+
+
+def _arenas(plan, side, rank, arenas, what, kinds=range(4)):
+    if len(arenas) != 4:
+        raise ValueError(f"{what} needs 4 arenas, got {len(arenas)}")
+    e = plan.arena_elems(side, rank)
+    return [_buf(arenas[k], e * ESIZE[k], f"{what}[{k}]") if k in kinds else _ptr(arenas[k])
+            for k in range(4)]
+
+
 def last_error():
     """Text of the calling thread's last error in the library ("" if none)."""
     lib()
@@ -310,6 +333,8 @@ def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None, failed=None):
     b = ParallelCfg(*dst.astuple())
     h = ctypes.c_void_p()
     pr = None if pair is None else np.ascontiguousarray(pair, np.int32)
+    if pr is not None and pr.shape != (b.tp * b.pp * b.dp,):
+        raise ValueError(f"pair needs one entry per new rank ({b.tp * b.pp * b.dp}), got {pr.shape}")
     fl = np.ascontiguousarray(failed if failed else [0], np.int32)
     opt = PlanOptions(None if pr is None else pr.ctypes.data, fl.ctypes.data,
                       len(failed) if failed else 0, rank, flags)
@@ -320,48 +345,98 @@ def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None, failed=None):
 
 def etc_cost_matrix(plan, which, out, stream=None):
     """out: device buffer of S*D (D*S for CM_COST) uint64 (an int64 tensor works)."""
-    _check(_lib.etc_cost_matrix(plan.handle, which, _ptr(out), _stream(stream)), "etc_cost_matrix")
+    _check(_lib.etc_cost_matrix(plan.handle, which, _buf(out, 8 * plan.S * plan.D, "out"),
+                                _stream(stream)), "etc_cost_matrix")
+
+
+def _in_range(plan, side, rank):
+    """Whether the plan has sizes for this rank (the library reports a bad one)."""
+    return 0 <= rank < (plan.S if side == SIDE_SRC else plan.D)
 
 
 def etc_pack(plan, src_rank, src_arenas, send_buf, stream=None):
-    arr = (ctypes.c_void_p * 4)(*[_ptr(x) for x in src_arenas])
-    _check(_lib.etc_pack(plan.handle, src_rank, ctypes.cast(arr, ctypes.c_void_p), _ptr(send_buf),
-                         _stream(stream)), "etc_pack")
+    """Tensors are checked against the plan's sizes (ValueError if short)."""
+    ok = _in_range(plan, SIDE_SRC, src_rank)
+    a = _arenas(plan, SIDE_SRC, src_rank, src_arenas, "src_arenas") if ok else \
+        [_ptr(x) for x in src_arenas]
+    need = plan.send_layout(src_rank)[3] if ok else 0
+    arr = (ctypes.c_void_p * 4)(*a)
+    _check(_lib.etc_pack(plan.handle, src_rank, ctypes.cast(arr, ctypes.c_void_p),
+                         _buf(send_buf, need, "send_buf"), _stream(stream)), "etc_pack")
+
+
+def _msgs(plan, dst_rank, msgs, kind=None):
+    """Message pointers of the S sources; tensors must hold that message."""
+    if len(msgs) != plan.S:
+        raise ValueError(f"need {plan.S} message pointers, got {len(msgs)}")
+    out = []
+    sized = _in_range(plan, SIDE_DST, dst_rank) and (kind is None or 0 <= kind < 4)
+    for s, x in enumerate(msgs):
+        if x is None or isinstance(x, int) or not sized:
+            out.append(_ptr(x))
+        elif kind is None:
+            out.append(_buf(x, int(plan.send_layout(s)[1][dst_rank]), f"msgs[{s}]"))
+        else:
+            out.append(_buf(x, int(plan.chunk_layout(s, kind)[0][dst_rank]), f"msgs[{s}]"))
+    return (ctypes.c_void_p * plan.S)(*out)
 
 
 def etc_unpack(plan, dst_rank, msgs, dst_arenas, stream=None):
-    """msgs: S entries (tensor, int pointer or None)."""
-    if len(msgs) != plan.S:
-        raise ValueError(f"need {plan.S} message pointers, got {len(msgs)}")
-    m = (ctypes.c_void_p * plan.S)(*[_ptr(x) for x in msgs])
-    arr = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
+    """msgs: S entries (tensor, int pointer or None).  Tensors are checked
+    against the plan's sizes (ValueError if short)."""
+    m = _msgs(plan, dst_rank, msgs)
+    a = _arenas(plan, SIDE_DST, dst_rank, dst_arenas, "dst_arenas") \
+        if _in_range(plan, SIDE_DST, dst_rank) else [_ptr(x) for x in dst_arenas]
+    arr = (ctypes.c_void_p * 4)(*a)
     _check(_lib.etc_unpack(plan.handle, dst_rank, ctypes.cast(m, ctypes.c_void_p),
                            ctypes.cast(arr, ctypes.c_void_p), _stream(stream)), "etc_unpack")
 
 
+def _home(plan, dst_rank):
+    if not _in_range(plan, SIDE_DST, dst_rank):
+        return -1
+    return int(plan.pairing()[dst_rank])
+
+
 def etc_refer(plan, dst_rank, src_arenas, dst_arenas, stream=None):
     """Refer: dst_rank's kept data from its paired source's arenas into its own."""
-    src = (ctypes.c_void_p * 4)(*[_ptr(x) for x in src_arenas])
-    dst = (ctypes.c_void_p * 4)(*[_ptr(x) for x in dst_arenas])
+    h = _home(plan, dst_rank)
+    sa = _arenas(plan, SIDE_SRC, h, src_arenas, "src_arenas") if h >= 0 else [_ptr(x) for x in src_arenas]
+    da = _arenas(plan, SIDE_DST, dst_rank, dst_arenas, "dst_arenas") if h >= 0 else \
+        [_ptr(x) for x in dst_arenas]
+    src = (ctypes.c_void_p * 4)(*sa)
+    dst = (ctypes.c_void_p * 4)(*da)
     _check(_lib.etc_refer(plan.handle, dst_rank, ctypes.cast(src, ctypes.c_void_p),
                           ctypes.cast(dst, ctypes.c_void_p), _stream(stream)), "etc_refer")
 
 
+def _kind_arena(plan, side, rank, kind, x, what):
+    if not (0 <= kind < 4) or rank < 0 or not _in_range(plan, side, rank):
+        return _ptr(x)
+    return _buf(x, plan.arena_elems(side, rank) * ESIZE[kind], what)
+
+
 def etc_refer_kind(plan, dst_rank, kind, src_arena, dst_arena, stream=None):
     """etc_refer for one state kind (that kind's arenas)."""
-    _check(_lib.etc_refer_kind(plan.handle, dst_rank, kind, _ptr(src_arena), _ptr(dst_arena),
+    h = _home(plan, dst_rank)
+    _check(_lib.etc_refer_kind(plan.handle, dst_rank, kind,
+                               _kind_arena(plan, SIDE_SRC, h, kind, src_arena, "src_arena"),
+                               _kind_arena(plan, SIDE_DST, dst_rank if h >= 0 else -1, kind, dst_arena,
+                                           "dst_arena"),
                                _stream(stream)), "etc_refer_kind")
 
 
 def etc_pack_kind(plan, src_rank, kind, src_arena, chunk_buf, stream=None):
-    _check(_lib.etc_pack_kind(plan.handle, src_rank, kind, _ptr(src_arena), _ptr(chunk_buf),
-                              _stream(stream)), "etc_pack_kind")
+    need = plan.chunk_layout(src_rank, kind)[2] if _in_range(plan, SIDE_SRC, src_rank) and \
+        0 <= kind < 4 else 0
+    _check(_lib.etc_pack_kind(plan.handle, src_rank, kind,
+                              _kind_arena(plan, SIDE_SRC, src_rank, kind, src_arena, "src_arena"),
+                              _buf(chunk_buf, need, "chunk_buf"), _stream(stream)), "etc_pack_kind")
 
 
 def etc_unpack_kind(plan, dst_rank, kind, msgs, dst_arena, stream=None):
     """msgs: S entries (tensor, int pointer or None), each in the chunk layout."""
-    if len(msgs) != plan.S:
-        raise ValueError(f"need {plan.S} message pointers, got {len(msgs)}")
-    m = (ctypes.c_void_p * plan.S)(*[_ptr(x) for x in msgs])
+    m = _msgs(plan, dst_rank, msgs, kind)
     _check(_lib.etc_unpack_kind(plan.handle, dst_rank, kind, ctypes.cast(m, ctypes.c_void_p),
-                                _ptr(dst_arena), _stream(stream)), "etc_unpack_kind")
+                                _kind_arena(plan, SIDE_DST, dst_rank, kind, dst_arena, "dst_arena"),
+                                _stream(stream)), "etc_unpack_kind")

@@ -1,5 +1,7 @@
 """GPU test helpers: device arenas filled with the seeded states at the
-oracle's layout, chunked bitwise comparison and sampled gathers."""
+oracle's layout, chunked bitwise comparison, whole send buffers expected
+from the oracle's message boxes, windows of the oracle's own migration at
+real shape, and sampled gathers."""
 from __future__ import annotations
 
 import sys
@@ -184,35 +186,156 @@ def sampled_origin_check(model, src, dst, d, dst_ar, src_ars, n=4096, seed=0, pa
         np.testing.assert_array_equal(got, want, err_msg=f"target {d} kind {k}")
 
 
-def check_messages(plan, model, src, dst, s, send, src_ar, n=4096, pair=None):
-    """Sampled message elements against the oracle's serialization."""
-    cnt, mb, dsp, _ = plan.send_layout(s)
-    rng = np.random.default_rng(s)
-    for d in np.nonzero(cnt)[0]:
-        npad = int(mb[d]) // 14
-        pos = np.unique(rng.integers(0, npad, n, dtype=np.int64)).astype(np.uint64)
-        so = oracle.msg_origin(model, src, dst, s, int(d), pos, pair=pair)
-        pad = so == np.uint64(2 ** 64 - 1)
-        sec = int(dsp[d])
-        for k in range(4):
-            got = gather(send[sec:sec + npad * ESIZE[k]], k, pos)
-            want = np.zeros_like(got)
-            if (~pad).any():
-                want[~pad] = gather(src_ar[k], k, so[~pad])
-            np.testing.assert_array_equal(got, want, err_msg=f"message {s}->{d} kind {k}")
-            sec += npad * ESIZE[k]
-
-
 def expected_dst(model, cfg, d, seed):
     ar = alloc(oracle.layout(model, cfg, d)[1])
     fill(model, cfg, d, ar, seed)
     return ar
 
 
-def share_run(w, plan, pair=None, check=True):
+SECTION = (0, 2, 6, 10)  # byte offset of kind k's section, in units of npad
+
+
+def expected_send(model, src, dst, s, seed, pair=None, failed=None, direct_refer=False):
+    """Source s's whole send buffer as it must be: the oracle's send layout and
+    message boxes (the wire format's positions) filled with the seeded values
+    of each box's logical elements; box padding and the gaps between messages
+    stay zero."""
+    cnt, mb, dsp, tot = oracle.send_layout(model, src, dst, s, pair=pair, failed=failed,
+                                           direct_refer=direct_refer)
+    buf = torch.zeros(max(int(tot), 1), dtype=torch.uint8, device=DEV)
+    fc = full_cols(model)
+    for d in np.nonzero(mb)[0]:
+        boxes, npad = oracle.message(model, src, dst, s, int(d), pair=pair, failed=failed,
+                                     direct_refer=direct_refer)
+        assert npad * 14 == int(mb[d])
+        base = buf.data_ptr() + int(dsp[d])
+        pieces = [dict(tensor=b["tensor"], r0=b["r0"], r1=b["r1"], c0=b["c0"], c1=b["c1"], off=b["moff"])
+                  for b in boxes]
+        synth.fill_device(pieces, fc, [base + npad * o for o in SECTION], seed, stream())
+    torch.cuda.synchronize()
+    return buf[:int(tot)]
+
+
+def check_send(plan, model, src, dst, s, send, seed, pair=None, failed=None, direct_refer=False):
+    """Every byte of source s's send buffer (messages, padding, gaps) against
+    expected_send; returns the number of non-empty messages."""
+    cnt, mb, dsp, tot = plan.send_layout(s)
+    ocnt, omb, odsp, otot = oracle.send_layout(model, src, dst, s, pair=pair, failed=failed,
+                                               direct_refer=direct_refer)
+    assert (cnt == ocnt).all() and (mb == omb).all() and (dsp == odsp).all() and tot == otot
+    assert send.numel() == tot
+    exp = expected_send(model, src, dst, s, seed, pair=pair, failed=failed, direct_refer=direct_refer)
+    assert equal(send, exp), f"send buffer of source {s}"
+    return int(np.count_nonzero(mb))
+
+
+def check_chunks(plan, model, src, dst, s, k, chunk, exp_send):
+    """Source s's kind-k chunk buffer against kind k's sections of its expected
+    full send buffer (a chunk message is that section byte for byte); the gaps
+    between chunk messages stay zero."""
+    cnt, mb, dsp, _ = plan.send_layout(s)
+    ccnt, cdsp, ctot = plan.chunk_layout(s, k)
+    exp = torch.zeros(max(int(ctot), 256), dtype=torch.uint8, device=DEV)
+    for d in np.nonzero(mb)[0]:
+        npad = int(mb[d]) // 14
+        assert int(ccnt[d]) == npad * ESIZE[k]
+        a = int(dsp[d]) + npad * SECTION[k]
+        exp[int(cdsp[d]):int(cdsp[d]) + int(ccnt[d])] = exp_send[a:a + int(ccnt[d])]
+    assert equal(chunk[:exp.numel()], exp), f"chunk buffer of source {s} kind {k}"
+
+
+def share_windows(model, src, dst, s0, d0, pair=None):
+    """Three contiguous windows of tensor ids that a share touches (tensors
+    of target d0's pieces or of source s0's messages): the first touched
+    tensor (the embedding when the share holds stage 0), the tensors of the
+    middle layer that s0's messages carry (of the target's layers if they
+    carry none), and those of the target's last layer together with every
+    touched tensor after it (final norm and head)."""
+    T = oracle.tensors(model)
+    held = {p["tensor"] for p in oracle.layout(model, dst, d0)[0]}
+    sent = set()
+    cnt = oracle.send_layout(model, src, dst, s0, pair=pair)[0]
+    for d in np.nonzero(cnt)[0]:
+        sent |= {b["tensor"] for b in oracle.message(model, src, dst, s0, int(d), pair=pair)[0]}
+    touched = held | sent
+
+    def layers(ids):
+        return sorted({T[t]["layer"] for t in ids if T[t]["layer"] >= 0})
+
+    def span(ly):
+        ids = [t for t in range(len(T)) if T[t]["layer"] == ly]
+        return min(ids), max(ids) + 1
+
+    first = min(touched)
+    out = [(first, first + 1)]
+    mid = layers(sent) or layers(held)
+    lo, hi = span(mid[len(mid) // 2])
+    if lo >= out[-1][1]:
+        out.append((lo, hi))
+    lo, hi = span(layers(held)[-1])
+    hi = max(max(touched) + 1, hi)
+    if lo >= out[-1][1]:
+        out.append((lo, hi))
+    return out
+
+
+def oracle_window_check(model, src, dst, seed, pair, resident, packed, d0, dev_send, dev_dst,
+                        windows, direct_refer=False):
+    """The oracle's own migration over windows of tensor ids, at real shape:
+    fresh lazily zeroed host arenas, the resident sources' pieces in the
+    window filled with the seeded values, materialize-then-cut for target d0
+    and the packed sources' messages; then the GPU's target pieces and
+    message boxes of those tensors byte for byte against it."""
+    fc = full_cols(model)
+    dl = oracle.layout(model, dst, d0)
+    for t_lo, t_hi in windows:
+        say(f"  oracle window: tensors [{t_lo}, {t_hi})")
+        hs = {}
+        for s in resident:
+            pieces, elems = oracle.layout(model, src, s)
+            hs[s] = [np.zeros(elems * e, np.uint8) for e in ESIZE]
+            synth.fill_host([p for p in pieces if t_lo <= p["tensor"] < t_hi], fc, hs[s], seed)
+        hd = [np.zeros(dl[1] * e, np.uint8) for e in ESIZE]
+        hb = {s: np.zeros(max(oracle.send_layout(model, src, dst, s, pair=pair,
+                                                 direct_refer=direct_refer)[3], 1), np.uint8)
+              for s in packed}
+        oracle.migrate(model, src, dst, hs, {d0: hd}, hb, t_lo, t_hi, pair=pair,
+                       direct_refer=direct_refer)
+        nb = 0
+        for p in dl[0]:
+            if not t_lo <= p["tensor"] < t_hi:
+                continue
+            n = (p["r1"] - p["r0"]) * (p["c1"] - p["c0"])
+            for k in range(4):
+                a, b = p["off"] * ESIZE[k], (p["off"] + n) * ESIZE[k]
+                assert np.array_equal(dev_dst[k][a:b].cpu().numpy(), hd[k][a:b]), \
+                    f"target {d0} tensor {p['tensor']} kind {k} vs the oracle"
+                nb += b - a
+        for s in packed:
+            cnt, mb, dsp, _ = oracle.send_layout(model, src, dst, s, pair=pair, direct_refer=direct_refer)
+            for d in np.nonzero(mb)[0]:
+                boxes, npad = oracle.message(model, src, dst, s, int(d), pair=pair,
+                                             direct_refer=direct_refer)
+                for x in boxes:
+                    if not t_lo <= x["tensor"] < t_hi:
+                        continue
+                    n = (x["r1"] - x["r0"]) * (x["c1"] - x["c0"])
+                    for k in range(4):
+                        a = int(dsp[d]) + npad * SECTION[k] + x["moff"] * ESIZE[k]
+                        b = a + n * ESIZE[k]
+                        assert np.array_equal(dev_send[s][a:b].cpu().numpy(), hb[s][a:b]), \
+                            f"message {s}->{d} tensor {x['tensor']} kind {k} vs the oracle"
+                        nb += b - a
+        say(f"    {nb / 1e9:.2f} GB equal to the oracle's")
+        del hs, hd, hb
+
+
+def share_run(w, plan, pair=None, check=True, windows=False):
     """Pack the share's source (and the sources feeding its target), unpack the
-    target; check messages and origins against the oracle and the whole target
-    against the seeded values."""
+    target; check every packed send buffer in full (expected from the
+    oracle's message boxes), with windows also three windows of tensors
+    against the oracle's own migration, sampled origins, and the whole
+    target against the seeded values."""
     s0 = w.pack_rank
     d0 = plan.process(w.unpack_rank)[1] if pair is not None else w.unpack_rank
     feeders = [int(s) for s in np.nonzero(plan.recv_counts(d0))[0]]
@@ -231,8 +354,13 @@ def share_run(w, plan, pair=None, check=True):
     etc.etc_unpack(plan, d0, msgs, dd)
     torch.cuda.synchronize()
     if check:
-        say("  sampled messages of source", s0)
-        check_messages(plan, w.model, w.src, w.dst, s0, send[s0], ds[s0], pair=pair)
+        for s in resident:
+            n = check_send(plan, w.model, w.src, w.dst, s, send[s], w.seed, pair=pair)
+            say(f"  send buffer of source {s}: {n} messages, {send[s].numel() / 1e9:.2f} GB, every byte")
+            torch.cuda.empty_cache()
+        if windows:
+            oracle_window_check(w.model, w.src, w.dst, w.seed, pair, resident, [s0], d0, send, dd,
+                                share_windows(w.model, w.src, w.dst, s0, d0, pair=pair))
         say("  sampled origins of target", d0)
         sampled_origin_check(w.model, w.src, w.dst, d0, dd, ds, pair=pair)
     del send

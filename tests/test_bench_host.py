@@ -42,6 +42,7 @@ def test_cpu_baseline_runs(pairing):
     out = bench.cpu_baseline(WORKLOADS["tiny-gpt"], pairing)
     assert out["kind"] == "oracle" and out["cores"] == min(16, bench.host_threads()) and out["unit"] == "GB/s"
     assert out["value"] > 0 and "layers 0-3" in out["sample"] and "on one thread" in out["sample"]
+    assert "4-layer sample of the share, not the whole share" in out["sample"]
 
 
 def test_oracle_threads_write_the_same_bytes():

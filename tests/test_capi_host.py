@@ -205,3 +205,63 @@ def test_chunk_calls_need_device_plan():
         with pytest.raises(etc.EtcError) as e:
             call()
         assert e.value.code == etc.ERR_INVALID_ARG
+
+
+def test_binding_checks_buffer_sizes():
+    """The binding refuses, before any library call, a torch tensor that is
+    not a contiguous GPU tensor or is smaller than the plan says (the kernels
+    would write past it), and a pairing of the wrong length."""
+    import torch
+    w = WORKLOADS["tiny-gpt"]
+    p = etc.etc_plan(w.model, w.src, w.dst, flags=HOST)
+    host = [torch.zeros(p.arena_elems(etc.SIDE_SRC, 0) * e, dtype=torch.uint8) for e in etc.ESIZE]
+    with pytest.raises(ValueError, match="GPU tensor"):
+        etc.etc_pack(p, 0, host, None)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        etc.etc_pack_kind(p, 0, 1, host[1], None)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        etc.etc_cost_matrix(p, etc.CM_ROUTE, torch.zeros(p.S * p.D, dtype=torch.int64))
+    with pytest.raises(ValueError, match="4 arenas"):
+        etc.etc_pack(p, 0, host[:3], None)
+    with pytest.raises(ValueError, match="message pointers"):
+        etc.etc_unpack(p, 0, [None] * (p.S - 1), [0, 0, 0, 0])
+    with pytest.raises(ValueError, match="one entry per new rank"):
+        etc.etc_plan(w.model, w.src, w.dst, pair=[0, 1, 2], flags=HOST)
+    # integer pointers pass through unchecked, and the library reports its own errors
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_pack(p, 0, [256] * 4, 256, stream=0)
+    assert e.value.code == etc.ERR_INVALID_ARG  # host-only plan: no device tables
+
+
+def test_binding_size_rule():
+    """The size rule itself, on stand-in tensors that report a GPU device:
+    exactly the plan's size passes, one byte less is refused."""
+    class Fake:
+        is_cuda = True
+
+        def __init__(self, n):
+            self.n = n
+
+        def is_contiguous(self):
+            return True
+
+        def numel(self):
+            return self.n
+
+        def element_size(self):
+            return 1
+
+        def data_ptr(self):
+            return 4096
+
+    assert etc._buf(Fake(100), 100, "x") == 4096
+    with pytest.raises(ValueError, match="holds 99 bytes; the plan needs 100"):
+        etc._buf(Fake(99), 100, "x")
+    w = WORKLOADS["tiny-gpt"]
+    p = etc.etc_plan(w.model, w.src, w.dst, flags=HOST)
+    e = p.arena_elems(etc.SIDE_SRC, 1)
+    ok = [Fake(e * k) for k in etc.ESIZE]
+    assert etc._arenas(p, etc.SIDE_SRC, 1, ok, "a") == [4096] * 4
+    short = ok[:3] + [Fake(e * 4 - 1)]
+    with pytest.raises(ValueError, match=r"a\[3\]"):
+        etc._arenas(p, etc.SIDE_SRC, 1, short, "a")

@@ -3,15 +3,16 @@ vocab 2^28 + 1 under the identity configuration TP1 PP1: the embedding is one
 contiguous run of 17 * (2^28 + 1) = 4,563,402,769 elements (64 GB over the
 four kinds), which the copy tables cut into rows of 2^31 elements and a ragged
 remainder.  Message elements at the cuts, at the padding and at random
-positions against the oracle's serialization; the target against the seeded
-values (identity: every element stays at its place).  Peak device memory
-about 128 GB."""
+positions against the oracle's serialization, then the whole message against
+the oracle's boxes filled with the seeded values; the target against the
+seeded values (identity: every element stays at its place).  Peak device
+memory about 128 GB."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_util import DEV, ESIZE, alloc, equal, expected_dst, gather, say, seeded_arenas
+from gpu_util import DEV, ESIZE, alloc, check_send, equal, expected_dst, gather, say, seeded_arenas
 from paper_2607_04749_amd import etc
 from paper_2607_04749_amd.workloads import GPT, ModelShape, Parallel
 
@@ -69,6 +70,9 @@ def test_pack_unpack_run_beyond_2_32_elements():
         assert equal(chunk[int(cdsp[0]):int(cdsp[0]) + int(ccnt[0])], send[sec:sec + npad * ESIZE[k]])
         del chunk
     del src
+    torch.cuda.empty_cache()
+    say("  the whole message, every byte")
+    check_send(plan, MODEL, CFG, CFG, 0, send, SEED)
     torch.cuda.empty_cache()
     say("  unpack, then the whole target against the seeded values")
     dst = alloc(plan.arena_elems(etc.SIDE_DST, 0))

@@ -1,16 +1,18 @@
 """Parity of the HIP path (through the C ABI) with the CPU oracle.
 
 Small workloads (micro models, Tiny GPT) are compared byte for byte over
-every message and every target arena.  Full-size workloads are compared on
-sampled elements the oracle computes one by one, and in full against the
-seeded values every target element must hold (an independent closed form);
-plus round trips and identity configurations."""
+every message and every target arena.  At full size every byte of every
+send buffer a test packs is compared with the oracle's message boxes filled
+with the seeded values, every target byte with the seeded values (an
+independent closed form), windows of tensors with the oracle's own
+migration run at real shape, and sampled elements with the oracle's
+per-element origins; plus round trips and identity configurations."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_util import (alloc, check_matrices, check_messages, emulate, equal, expected_dst,
+from gpu_util import (alloc, check_matrices, check_send, emulate, equal, expected_dst,
                       full_compare, say, sampled_origin_check, seeded_arenas, share_run)
 from helpers import host_arenas
 from micro import MICRO_MODELS, cfg_pairs
@@ -89,7 +91,8 @@ def test_gpt_1_3b_full_emulation(pairing):
             assert equal(dd[d][k], exp[k]), f"target {d} kind {k} vs seeded values"
         del exp
     for s in range(w.src.world):
-        check_messages(plan, w.model, w.src, w.dst, s, send[s], ds[s], pair=pr)
+        n = check_send(plan, w.model, w.src, w.dst, s, send[s], w.seed, pair=pr)
+        say(f"  send buffer of source {s}: {n} messages, every byte")
     del send
     torch.cuda.empty_cache()
     if pr is not None:
@@ -108,13 +111,18 @@ def test_gpt_1_3b_full_emulation(pairing):
 def test_share_at_full_size(wl, pairing):
     """One source rank's pack and one target rank's unpack at real shape.  With
     the oracle's sketch this is the launch configuration the benchmark times
-    (for these workloads the library's own sketch finds the same pairing)."""
+    (for these workloads the library's own sketch finds the same pairing).
+    Every send buffer packed is compared in full: the 13B source 0 packs
+    messages to targets 0 and 1, and under the identity pairing also the
+    norms message to target 4.  The oracle's own migration checks three
+    windows of tensors in the benchmark's configuration, and under the
+    identity pairing at 13B."""
     w = WORKLOADS[wl]
     pr = oracle_sketch(w) if pairing == "sketch" else None
     say(wl, "share", w.src, "->", w.dst, pairing, "process", w.pack_rank)
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr)
     check_matrices(plan, w.model, w.src, w.dst, pr)
-    share_run(w, plan, pair=pr)
+    share_run(w, plan, pair=pr, windows=pairing == "sketch" or wl == "llama-13b")
 
 
 def test_max_peers_full_emulation():
@@ -141,7 +149,7 @@ def test_error_paths_on_device():
         etc.etc_pack(plan, 0, [ds[0].data_ptr() + 2] + ds[1:], buf)
     assert e.value.code == etc.ERR_ALIGN
     with pytest.raises(etc.EtcError) as e:
-        etc.etc_pack(plan, 1, ds, buf)  # source 1 is not built into a rank-0 plan
+        etc.etc_pack(plan, 1, [x.data_ptr() for x in ds], buf.data_ptr())  # not built into a rank-0 plan
     assert e.value.code == etc.ERR_RANK
     with pytest.raises(etc.EtcError) as e:
         etc.etc_unpack(plan, 0, [None] * plan.S, alloc(plan.arena_elems(etc.SIDE_DST, 0)))
@@ -150,6 +158,15 @@ def test_error_paths_on_device():
     with pytest.raises(etc.EtcError) as e:
         etc.etc_cost_matrix(plan, 9, out)
     assert e.value.code == etc.ERR_INVALID_ARG
+    # the binding refuses short tensors before the library sees them
+    with pytest.raises(ValueError, match="the plan needs"):
+        etc.etc_pack(plan, 0, ds, buf[:plan.send_layout(0)[3] - 1])
+    with pytest.raises(ValueError, match="the plan needs"):
+        etc.etc_pack(plan, 0, [ds[0][:-2]] + ds[1:], buf)
+    with pytest.raises(ValueError, match="the plan needs"):
+        etc.etc_unpack(plan, 0, [None] * plan.S, [x[:-4] for x in alloc(plan.arena_elems(etc.SIDE_DST, 0))])
+    with pytest.raises(ValueError, match="the plan needs"):
+        etc.etc_cost_matrix(plan, etc.CM_ROUTE, out[:-1])
     with pytest.raises(etc.EtcError) as e:
         etc.etc_cost_matrix(plan, etc.CM_ROUTE, out.data_ptr() + 4)
     assert e.value.code == etc.ERR_ALIGN

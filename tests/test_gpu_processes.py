@@ -53,9 +53,10 @@ def _run(model, a, b, seed, failed=None, flags=etc.PLAN_SKETCH):
             continue
         send[s] = torch.full((max(pl.send_layout(s)[3], 256),), 0x5A, dtype=torch.uint8, device=DEV)
         etc.etc_pack(pl, s, ds[s], send[s])
-        if S > 1:  # a process's plan serves its own ranks only
+        if S > 1:  # a process's plan serves its own ranks only (raw pointers: the
+            # library's own check, not the binding's size check, must refuse it)
             with pytest.raises(etc.EtcError) as e:
-                etc.etc_pack(pl, (s + 1) % S, ds[s], send[s])
+                etc.etc_pack(pl, (s + 1) % S, [x.data_ptr() for x in ds[s]], send[s].data_ptr())
             assert e.value.code == etc.ERR_RANK
     dd = {}
     for p, pl in enumerate(plans):
@@ -72,7 +73,7 @@ def _run(model, a, b, seed, failed=None, flags=etc.PLAN_SKETCH):
             etc.etc_refer(pl, d, ds[s], dd[d])
         if D > 1:
             with pytest.raises(etc.EtcError) as e:
-                etc.etc_unpack(pl, (d + 1) % D, msgs, dd[d])
+                etc.etc_unpack(pl, (d + 1) % D, msgs, [x.data_ptr() for x in dd[d]])
             assert e.value.code == etc.ERR_RANK
     torch.cuda.synchronize()
     assert sorted(dd) == list(range(D))

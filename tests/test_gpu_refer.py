@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import (DEV, alloc, equal, expected_dst, full_compare, sampled_origin_check, say,
+from gpu_util import (DEV, alloc, check_send, equal, expected_dst, full_compare, sampled_origin_check, say,
                       seeded_arenas)
 from micro import MICRO_MODELS, cfg_pairs
 from paper_2607_04749_amd import etc
@@ -81,6 +81,9 @@ def test_share_direct_refer(wl):
     etc.etc_refer(plan, d0, src[s0], dst)
     etc.etc_unpack(plan, d0, msgs, dst)
     torch.cuda.synchronize()
+    for s in feeders:
+        n = check_send(plan, w.model, w.src, w.dst, s, send[s], w.seed, pair=pr, direct_refer=True)
+        say(f"  send buffer of source {s}: {n} messages, every byte")
     say("  sampled origins")
     sampled_origin_check(w.model, w.src, w.dst, d0, dst, src, pair=pr)
     del send
