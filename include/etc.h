@@ -20,6 +20,8 @@
  * This library is the data-parallel hot path of that migration on one GPU:
  *   etc_sketch       host: the migration sketch (pairing of new and old ranks)
  *   etc_plan         host: layouts, routing, message layout, tile tables
+ *   etc_plan_static  the same, device tables in a static array (no device
+ *                    allocation)
  *   etc_plan_defrag  host: virtual rank allocator and the coalesced pairing
  *   etc_plan_message, etc_plan_refer   host: the instruction lists
  *   etc_cost_matrix  device: byte matrices over every (source, target) pair
@@ -233,6 +235,35 @@ typedef struct {
  * NOMEM, HIP. */
 ETC_API int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src,
                      const etc_parallel_cfg* dst, const etc_plan_options* opt, etc_plan_t** out);
+
+/* Size of the library's static device table array (per GPU), bytes. */
+enum { ETC_STATIC_TABLE_BYTES = 4 << 20 };
+
+/* etc_plan for callers that cannot allocate device memory (code that runs
+ * while hipMalloc is forbidden: a serving loop, a harness that owns all of
+ * HBM).  Same arguments, plan and results as etc_plan, but the device tables
+ * are written into a static array of ETC_STATIC_TABLE_BYTES bytes that the
+ * library holds on each GPU until the process ends, instead of memory of
+ * their own: no hipMalloc, hipFree or other device allocation is made (host
+ * memory for the plan itself is still allocated).  Every device call
+ * (etc_cost_matrix, etc_pack, etc_unpack, the one-kind calls, etc_refer)
+ * then reads the tables from that array.
+ * One array per GPU, shared by every call: each etc_plan_static call on a
+ * device first waits until the device is idle (hipDeviceSynchronize), then
+ * replaces the tables; from then on device calls with a static plan built
+ * earlier on that device fail with INVALID_ARG (the plan's host queries
+ * still work; free it as usual).  Device calls of the live static plan may
+ * run from any threads and streams.  Do not call it while a stream of the
+ * device is being captured, and do not replay a graph captured with an
+ * earlier static plan after a later call: its launches would read the new
+ * tables.
+ * Errors: as etc_plan; INVALID_ARG also for ETC_PLAN_HOST_ONLY; UNSUPPORTED
+ * when the tables need more than ETC_STATIC_TABLE_BYTES (a plan with
+ * ETC_ALL_RANKS for Llama-70B TP8xPP8 -> TP8xPP4 needs about 0.6 MB; a
+ * per-process plan far less). */
+ETC_API int etc_plan_static(const etc_model_desc* model, const etc_parallel_cfg* src,
+                            const etc_parallel_cfg* dst, const etc_plan_options* opt,
+                            etc_plan_t** out);
 
 /* Virtual rank allocator (Sec. III-E, Algorithm 2): de-fragment the devices
  * after the plan's migration.  The migration leaves new rank d on the device

@@ -5,8 +5,11 @@
 #include <algorithm>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <new>
+#include <shared_mutex>
 #include <string>
+#include <vector>
 
 #include "copy_geom.hpp"
 #include "etc.h"
@@ -29,8 +32,50 @@ int hip_fail(hipError_t e, const char* what) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// ---------------------------------------------------------------------------
+// Static device tables (etc_plan_static): a file-scope device array that the
+// library never allocates or frees.  Each GPU holds its own copy at its own
+// address, looked up once per device with that device current; host code
+// uses only that address (the array's name is a host-side stand-in).  One
+// static plan per device is live at a time: g_static_gen counts the calls
+// per device, and a plan built by an earlier call is refused.  Device calls
+// of a static plan hold the lock shared from the check to the launch, and
+// etc_plan_static holds it exclusively while it waits for the device and
+// rewrites the array, so no launch ever reads a half-written table.
+
+__device__ __align__(256) unsigned char scratch[ETC_STATIC_TABLE_BYTES];
+
+struct StaticSlot {
+  void* ptr = nullptr;  // device address of `scratch` on this device
+  uint64_t gen = 0;     // etc_plan_static calls on this device so far
+};
+std::shared_mutex g_static_mu;
+std::vector<StaticSlot> g_static;  // by device ordinal; guarded by g_static_mu
+
+// The array's address on `dev` (current device), looked up on first use.
+// Caller holds g_static_mu exclusively.
+hipError_t static_slot(int dev, StaticSlot** out) {
+  if (size_t(dev) >= g_static.size()) g_static.resize(size_t(dev) + 1);
+  StaticSlot& s = g_static[size_t(dev)];
+  if (!s.ptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    s.ptr = p;
+  }
+  *out = &s;
+  return hipSuccess;
+}
+
 void release_device(etc_plan_t* P) {
   if (P->device < 0) return;
+  if (P->static_gen) {  // tables in the static array: nothing to free
+    P->d_boxes = nullptr;
+    P->d_route_tensors = nullptr;
+    P->d_home = nullptr;
+    P->d_failed = nullptr;
+    return;
+  }
   int prev = -1;
   const bool have_prev = hipGetDevice(&prev) == hipSuccess;
   if (prev != P->device) (void)hipSetDevice(P->device);
@@ -58,6 +103,27 @@ int check_device_plan(const etc_plan_t* P) {
   return ETC_OK;
 }
 
+// Held by every device call from its checks to its launch: shared for a
+// static plan (whose tables must still be the live ones), nothing otherwise.
+class DeviceCallGuard {
+ public:
+  explicit DeviceCallGuard(const etc_plan_t* P) {
+    if (P && P->static_gen) lock_ = std::shared_lock<std::shared_mutex>(g_static_mu);
+  }
+  // ETC_OK, or the error of a static plan replaced by a later etc_plan_static
+  int check(const etc_plan_t* P) const {
+    if (!P || !P->static_gen) return ETC_OK;
+    const uint64_t live = size_t(P->device) < g_static.size() ? g_static[size_t(P->device)].gen : 0;
+    if (live != P->static_gen)
+      return fail(ETC_ERR_INVALID_ARG, "the static device tables of this plan were replaced by a later "
+                                       "etc_plan_static on device " + std::to_string(P->device));
+    return ETC_OK;
+  }
+
+ private:
+  std::shared_lock<std::shared_mutex> lock_;
+};
+
 // Roles of process p: it holds old rank p (p < S) and becomes the new rank
 // paired with it; processes S, S+1, ... take the unpaired new ranks in order.
 void process_roles(const etc_plan_t* P, int p, int* src_rank, int* dst_rank) {
@@ -80,52 +146,61 @@ int num_processes(const etc_plan_t* P) {
   return P->src.world() + unpaired;
 }
 
-int upload(etc_plan_t* P, int rank) {
+// Host side of the device tables: cut the routed boxes of the process's
+// launches (every launch with ETC_ALL_RANKS) into tiles, in launch order.
+int build_copy_tables(etc_plan_t* P, int rank, std::vector<etc::CopyBox>* all) {
   using namespace etc;
   const int S = P->src.world(), D = P->dst.world();
   int my_src = -1, my_dst = -1;
   if (rank != ETC_ALL_RANKS) process_roles(P, rank, &my_src, &my_dst);
-  hipError_t e = hipGetDevice(&P->device);
-  if (e != hipSuccess) {
-    P->device = -1;
-    return hip_fail(e, "hipGetDevice");
-  }
-  std::vector<CopyBox> all;
   for (int s = 0; s < S; ++s) {
     if (rank != ETC_ALL_RANKS && my_src != s) continue;
     CopyTable& t = P->pack_tab[s];
     auto v = build_pack_boxes(*P, s, &t.peers, &t.bytes);
-    t.first = uint32_t(all.size());
+    t.first = uint32_t(all->size());
     t.nbox = uint32_t(v.size() - 1);
     t.ntiles = v.back().tile0;
     t.built = true;
-    all.insert(all.end(), v.begin(), v.end());
+    all->insert(all->end(), v.begin(), v.end());
   }
   for (int d = 0; d < D; ++d) {
     if (rank != ETC_ALL_RANKS && my_dst != d) continue;
     CopyTable& t = P->refer_tab[d];
     auto v = build_refer_boxes(*P, d, &t.bytes);
-    t.first = uint32_t(all.size());
+    t.first = uint32_t(all->size());
     t.nbox = uint32_t(v.size() - 1);
     t.ntiles = v.back().tile0;
     t.built = true;
-    all.insert(all.end(), v.begin(), v.end());
+    all->insert(all->end(), v.begin(), v.end());
   }
   for (int d = 0; d < D; ++d) {
     if (rank != ETC_ALL_RANKS && my_dst != d) continue;
     CopyTable& t = P->unpack_tab[d];
     auto v = build_unpack_boxes(*P, d, &t.peers, &t.bytes);
-    t.first = uint32_t(all.size());
+    t.first = uint32_t(all->size());
     t.nbox = uint32_t(v.size() - 1);
     t.ntiles = v.back().tile0;
     t.built = true;
-    all.insert(all.end(), v.begin(), v.end());
+    all->insert(all->end(), v.begin(), v.end());
   }
   // the copy kernels launch one workgroup per sub-chunk of every tile
   for (const auto* tabs : {&P->pack_tab, &P->unpack_tab, &P->refer_tab})
     for (const CopyTable& t : *tabs)
       if (uint64_t(t.ntiles) * kSubPerTile > uint64_t(INT32_MAX))
         return fail(ETC_ERR_UNSUPPORTED, "a rank's copy needs more than 2^31 - 1 GPU workgroups");
+  return ETC_OK;
+}
+
+int upload(etc_plan_t* P, int rank) {
+  using namespace etc;
+  hipError_t e = hipGetDevice(&P->device);
+  if (e != hipSuccess) {
+    P->device = -1;
+    return hip_fail(e, "hipGetDevice");
+  }
+  std::vector<CopyBox> all;
+  int rc = build_copy_tables(P, rank, &all);
+  if (rc) return rc;
   if (!all.empty()) {
     e = hipMalloc(&P->d_boxes, all.size() * sizeof(CopyBox));
     if (e != hipSuccess) return fail(ETC_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
@@ -151,6 +226,50 @@ int upload(etc_plan_t* P, int rank) {
                   hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy (failed ranks)");
   }
+  return ETC_OK;
+}
+
+// The same device tables written into the current device's static array:
+// copy boxes, tensor table, pairing, failed ranks, each at a multiple of 256
+// bytes.  No device memory is allocated.
+int upload_static(etc_plan_t* P, int rank) {
+  using namespace etc;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::vector<CopyBox> all;
+  int rc = build_copy_tables(P, rank, &all);
+  if (rc) return rc;
+  auto up = [](size_t n) { return (n + 255) / 256 * 256; };
+  const size_t o_rt = up(all.size() * sizeof(CopyBox));
+  const size_t o_home = o_rt + up(P->route_tensors.size() * sizeof(RouteTensor));
+  const size_t o_failed = o_home + up(P->home.size() * sizeof(int32_t));
+  const size_t total = o_failed + P->failed_bits.size() * sizeof(uint32_t);
+  if (total > size_t(ETC_STATIC_TABLE_BYTES))
+    return fail(ETC_ERR_UNSUPPORTED, "the plan's device tables need " + std::to_string(total) +
+                                         " bytes; etc_plan_static holds at most " +
+                                         std::to_string(int(ETC_STATIC_TABLE_BYTES)) +
+                                         " (ETC_STATIC_TABLE_BYTES); use etc_plan, or a plan per process");
+  std::vector<unsigned char> img(std::max<size_t>(total, 1), 0);
+  std::memcpy(img.data(), all.data(), all.size() * sizeof(CopyBox));
+  std::memcpy(img.data() + o_rt, P->route_tensors.data(), P->route_tensors.size() * sizeof(RouteTensor));
+  std::memcpy(img.data() + o_home, P->home.data(), P->home.size() * sizeof(int32_t));
+  std::memcpy(img.data() + o_failed, P->failed_bits.data(), P->failed_bits.size() * sizeof(uint32_t));
+  std::unique_lock<std::shared_mutex> lock(g_static_mu);
+  StaticSlot* slot = nullptr;
+  if ((e = static_slot(dev, &slot)) != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (static tables)");
+  // the previous static plan's launches may still read the array
+  if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  ++slot->gen;  // from here on, earlier static plans of this device are refused
+  if ((e = hipMemcpy(slot->ptr, img.data(), img.size(), hipMemcpyHostToDevice)) != hipSuccess)
+    return hip_fail(e, "hipMemcpy (static tables)");
+  unsigned char* base = static_cast<unsigned char*>(slot->ptr);
+  P->device = dev;
+  P->static_gen = slot->gen;
+  P->d_boxes = all.empty() ? nullptr : reinterpret_cast<CopyBox*>(base);
+  P->d_route_tensors = reinterpret_cast<RouteTensor*>(base + o_rt);
+  P->d_home = reinterpret_cast<int32_t*>(base + o_home);
+  P->d_failed = P->failed_bits.empty() ? nullptr : reinterpret_cast<uint32_t*>(base + o_failed);
   return ETC_OK;
 }
 
@@ -219,8 +338,14 @@ int etc_sketch(const uint64_t* cost, int M, int N, int32_t* pair, uint64_t* tota
   return ETC_OK;
 }
 
-int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
-             const etc_plan_options* opt, etc_plan_t** out) {
+}  // extern "C"
+
+namespace {
+
+// etc_plan and etc_plan_static: the same plan, with its device tables in
+// memory of their own (hipMalloc) or in the device's static array.
+int make_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
+              const etc_plan_options* opt, etc_plan_t** out, bool in_static) {
   if (!out) return fail(ETC_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (!model || !src || !dst) return fail(ETC_ERR_INVALID_ARG, "model, src and dst must not be NULL");
@@ -280,8 +405,10 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
     P->pack_tab.resize(S);
     P->unpack_tab.resize(D);
     P->refer_tab.resize(D);
+    if (in_static && (flags & ETC_PLAN_HOST_ONLY))
+      return fail(ETC_ERR_INVALID_ARG, "etc_plan_static builds device tables: ETC_PLAN_HOST_ONLY is not allowed");
     if (!(flags & ETC_PLAN_HOST_ONLY)) {
-      const int rc = upload(P.get(), rank);
+      const int rc = in_static ? upload_static(P.get(), rank) : upload(P.get(), rank);
       if (rc != ETC_OK) {
         release_device(P.get());
         return rc;
@@ -297,6 +424,20 @@ int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc
   *out = P.release();
   g_last_error.clear();
   return ETC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int etc_plan(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
+             const etc_plan_options* opt, etc_plan_t** out) {
+  return make_plan(model, src, dst, opt, out, false);
+}
+
+int etc_plan_static(const etc_model_desc* model, const etc_parallel_cfg* src, const etc_parallel_cfg* dst,
+                    const etc_plan_options* opt, etc_plan_t** out) {
+  return make_plan(model, src, dst, opt, out, true);
 }
 
 int etc_plan_defrag(const etc_plan_t* P, int mode, int32_t* placement, int32_t* ops, int* nops,
@@ -447,6 +588,8 @@ int etc_plan_refer(const etc_plan_t* P, int d, etc_instruction* out, int cap, in
 int etc_cost_matrix(const etc_plan_t* P, int which, uint64_t* d_out, void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (which < ETC_CM_ROUTE || which > ETC_CM_COST) return fail(ETC_ERR_INVALID_ARG, "bad matrix selector");
   if (!d_out) return fail(ETC_ERR_INVALID_ARG, "d_out is NULL");
   if (!aligned(d_out, 8)) return fail(ETC_ERR_ALIGN, "d_out is not 8-byte aligned");
@@ -464,6 +607,8 @@ int etc_cost_matrix(const etc_plan_t* P, int which, uint64_t* d_out, void* strea
 int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* send_buf, void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (s < 0 || s >= P->src.world()) return fail(ETC_ERR_RANK, "source rank out of range");
   const etc::CopyTable& t = P->pack_tab[s];
   if (!t.built) return fail(ETC_ERR_RANK, "source rank " + std::to_string(s) + " is not built into this plan");
@@ -485,6 +630,8 @@ int etc_pack(const etc_plan_t* P, int s, const void* const src_arena[4], void* s
 int etc_unpack(const etc_plan_t* P, int d, const void* const* msg, void* const dst_arena[4], void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
   const etc::CopyTable& t = P->unpack_tab[d];
   if (!t.built) return fail(ETC_ERR_RANK, "target rank " + std::to_string(d) + " is not built into this plan");
@@ -529,6 +676,8 @@ int etc_pack_kind(const etc_plan_t* P, int s, int kind, const void* src_arena, v
                   void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
   if (s < 0 || s >= P->src.world()) return fail(ETC_ERR_RANK, "source rank out of range");
   const etc::CopyTable& t = P->pack_tab[s];
@@ -553,6 +702,8 @@ int etc_unpack_kind(const etc_plan_t* P, int d, int kind, const void* const* msg
                     void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
   if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
   const etc::CopyTable& t = P->unpack_tab[d];
@@ -580,6 +731,8 @@ int etc_refer(const etc_plan_t* P, int d, const void* const src_arena[4], void* 
               void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
   const etc::CopyTable& t = P->refer_tab[d];
   if (!t.built) return fail(ETC_ERR_RANK, "target rank " + std::to_string(d) + " is not built into this plan");
@@ -598,6 +751,8 @@ int etc_refer_kind(const etc_plan_t* P, int d, int kind, const void* src_arena, 
                    void* stream) {
   int rc = check_device_plan(P);
   if (rc) return rc;
+  const DeviceCallGuard guard(P);
+  if ((rc = guard.check(P))) return rc;
   if (kind < 0 || kind >= ETC_NUM_KINDS) return fail(ETC_ERR_INVALID_ARG, "bad kind");
   if (d < 0 || d >= P->dst.world()) return fail(ETC_ERR_RANK, "target rank out of range");
   const etc::CopyTable& t = P->refer_tab[d];

@@ -184,6 +184,9 @@ struct etc_plan_s {
 
   // device side
   int device = -1;
+  // non-zero: the device tables live in the library's static array of that
+  // device (etc_plan_static), written by its static_gen-th call there
+  uint64_t static_gen = 0;
   etc::RouteTensor* d_route_tensors = nullptr;
   int32_t* d_home = nullptr;  // device copy of home (D entries)
   uint32_t* d_failed = nullptr;  // device copy of failed_bits

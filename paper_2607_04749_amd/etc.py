@@ -29,6 +29,7 @@ PLAN_DIRECT_REFER = 4
 OK, ERR_INVALID_ARG, ERR_INDIVISIBLE, ERR_RANK, ERR_ALIGN, ERR_UNSUPPORTED, ERR_NOMEM, ERR_HIP = \
     0, -1, -2, -3, -4, -5, -6, -7
 ERR_UNRECOVERABLE = -8
+STATIC_TABLE_BYTES = 4 << 20
 COST_INF = 1 << 50
 MAX_PEERS = 256
 DEFRAG_NONE, DEFRAG_OCCUPANCY, DEFRAG_EFFICIENCY = 0, 1, 2
@@ -92,6 +93,7 @@ def _load():
     L.etc_plan.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(ParallelCfg),
                            ctypes.POINTER(ParallelCfg), ctypes.POINTER(PlanOptions),
                            ctypes.POINTER(vp)]
+    L.etc_plan_static.argtypes = L.etc_plan.argtypes
     L.etc_sketch.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, u64p]
     L.etc_plan_pairing.argtypes = [vp, vp]
     L.etc_refer.argtypes = [vp, ctypes.c_int, vp, vp, vp]
@@ -328,6 +330,18 @@ def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None, failed=None):
     vocab, max_pos, tied, flags); src/dst: objects with astuple() (tp, pp, dp);
     pair: None (identity), or D entries (old rank per new rank, -1 = none);
     failed: old ranks whose states are lost."""
+    return _make_plan(_lib.etc_plan, "etc_plan", model, src, dst, rank, flags, pair, failed)
+
+
+def etc_plan_static(model, src, dst, rank=ALL_RANKS, flags=0, pair=None, failed=None):
+    """etc_plan with the device tables in the library's static array (no
+    device allocation); a later call on the same GPU retires this plan's
+    device calls."""
+    return _make_plan(_lib.etc_plan_static, "etc_plan_static", model, src, dst, rank, flags, pair,
+                      failed)
+
+
+def _make_plan(call, name, model, src, dst, rank, flags, pair, failed):
     m = ModelDesc(*model.astuple())
     a = ParallelCfg(*src.astuple())
     b = ParallelCfg(*dst.astuple())
@@ -338,8 +352,8 @@ def etc_plan(model, src, dst, rank=ALL_RANKS, flags=0, pair=None, failed=None):
     fl = np.ascontiguousarray(failed if failed else [0], np.int32)
     opt = PlanOptions(None if pr is None else pr.ctypes.data, fl.ctypes.data,
                       len(failed) if failed else 0, rank, flags)
-    _check(_lib.etc_plan(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), ctypes.byref(opt),
-                         ctypes.byref(h)), "etc_plan")
+    _check(call(ctypes.byref(m), ctypes.byref(a), ctypes.byref(b), ctypes.byref(opt), ctypes.byref(h)),
+           name)
     return Plan(h, model, src, dst, rank)
 
 

@@ -265,3 +265,15 @@ def test_binding_size_rule():
     short = ok[:3] + [Fake(e * 4 - 1)]
     with pytest.raises(ValueError, match=r"a\[3\]"):
         etc._arenas(p, etc.SIDE_SRC, 1, short, "a")
+
+
+def test_static_plan_refuses_host_only():
+    """etc_plan_static exists to place device tables; asking it for a
+    host-only plan is refused before any device call."""
+    w = WORKLOADS["tiny-gpt"]
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan_static(w.model, w.src, w.dst, flags=HOST)
+    assert e.value.code == etc.ERR_INVALID_ARG and "HOST_ONLY" in str(e.value)
+    assert etc.STATIC_TABLE_BYTES == 4 << 20
+    hdr = open(os.path.join(ROOT, "include", "etc.h")).read()
+    assert re.search(r"ETC_STATIC_TABLE_BYTES = 4 << 20", hdr)
