@@ -57,7 +57,7 @@ def log(*a):
 
 def kernel_hash():
     h = hashlib.sha256()
-    for f in ("copy.hip", "copy_geom.hpp", "etc_internal.hpp", "tiles.hip", "route.hpp"):
+    for f in ("copy.hip", "copy_geom.hpp", "copy_desc.hpp", "tiles.hip", "route.hpp"):
         with open(os.path.join(ROOT, "paper_2607_04749_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

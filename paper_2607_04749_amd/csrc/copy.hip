@@ -11,7 +11,9 @@
 // fp32 kind, one 16-byte vector per lane; 512 B of bf16).  A launch of all
 // four kinds (pack, unpack, Refer) gives each workgroup one sub-chunk of
 // every kind, copied kind after kind; a launch of one kind (state chunking)
-// gives each workgroup kKindGroup consecutive sub-chunks of that kind.
+// gives each workgroup kind_group consecutive sub-chunks of that kind, each a
+// full wavefront of vectors (kind_sub_elems: 1 KB, 512 bf16 elements or 256
+// fp32 ones), 8 KB per workgroup.
 // Either way a workgroup finds its tile's descriptor once (a binary search of
 // the tile table, scalar loads) and then moves a few KB.  The hardware
 // dispatches the workgroups in index order, so the whole GPU advances
@@ -23,8 +25,9 @@
 // nothing is reused.
 #include <hip/hip_runtime.h>
 
+#include "copy_desc.hpp"
 #include "copy_geom.hpp"
-#include "etc_internal.hpp"
+#include "etc.h"
 
 namespace etc {
 
@@ -71,18 +74,20 @@ struct KindTile {
 // ---------------------------------------------------------------------------
 // All four kinds: one sub-chunk of each kind per workgroup.
 
-template <bool kPack, int kKind>
+// Sub-chunk j (kSub elements) of one kind of a tile.
+template <bool kPack, int kKind, uint32_t kSub>
 __device__ __forceinline__ void copy_sub_kind(const CopyArgs& a, const CopyBox& b, char* mbase,
                                               const TileGeom& g, uint32_t j) {
   using KT = KindTile<kPack, kKind>;
   using E = typename KT::E;
   constexpr int es = KT::es;
+  static_assert(kSub * es / 16 <= kSubThreads, "at most one vector per lane");
   const KT k(a, b, mbase, g);
   uint32_t lo, hi;
   if (sub_vectors(b, g, es)) {
     constexpr uint32_t vw = 16 / es;
     const uint32_t vpr = g.nc / vw;
-    sub_range(j, kSubElems / vw, g.nr * vpr, &lo, &hi);
+    sub_range(j, kSub / vw, g.nr * vpr, &lo, &hi);
     const uint32_t i = lo + threadIdx.x;  // at most one vector per lane
     if (i < hi) {
       const uint32_t r = g.nr == 1 ? 0 : i / vpr;
@@ -92,7 +97,7 @@ __device__ __forceinline__ void copy_sub_kind(const CopyArgs& a, const CopyBox& 
           reinterpret_cast<u32x4*>(k.dst + r * k.dld + uint64_t(c) * 16));
     }
   } else {
-    sub_range(j, kSubElems, g.nr * g.nc, &lo, &hi);
+    sub_range(j, kSub, g.nr * g.nc, &lo, &hi);
     const E* S = reinterpret_cast<const E*>(k.src);
     E* D = reinterpret_cast<E*>(k.dst);
     for (uint32_t i = lo + threadIdx.x; i < hi; i += kSubThreads) {
@@ -110,25 +115,27 @@ __global__ __launch_bounds__(kSubThreads) void copy_sub_kernel(CopyArgs a) {
   const CopyBox b = a.boxes[bi];
   const TileGeom g = tile_geom(b, t, a.boxes[bi + 1].tile0);
   char* mbase = a.peer[b.peer];
-  copy_sub_kind<kPack, 0>(a, b, mbase, g, j);
-  copy_sub_kind<kPack, 1>(a, b, mbase, g, j);
-  copy_sub_kind<kPack, 2>(a, b, mbase, g, j);
-  copy_sub_kind<kPack, 3>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 0, kSubElems>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 1, kSubElems>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 2, kSubElems>(a, b, mbase, g, j);
+  copy_sub_kind<kPack, 3, kSubElems>(a, b, mbase, g, j);
 }
 
 // ---------------------------------------------------------------------------
-// One kind: kKindGroup consecutive sub-chunks of one tile per workgroup.
+// One kind: kind_group(es) consecutive sub-chunks of kind_sub_elems(es)
+// elements of one tile per workgroup.
 
 template <bool kPack, int kKind>
 __device__ __forceinline__ void copy_kind_group(const CopyArgs& a) {
-  constexpr uint32_t groups = kSubPerTile / kKindGroup;
+  constexpr int es = kKind == 0 ? 2 : 4;
+  constexpr uint32_t sub = kind_sub_elems(es), grp = kind_group(es), groups = kind_wg_per_tile(es);
   const uint32_t t = blockIdx.x / groups, q = blockIdx.x % groups;
   const uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
   const CopyBox b = a.boxes[bi];
   const TileGeom g = tile_geom(b, t, a.boxes[bi + 1].tile0);
   char* mbase = a.peer[b.peer];
 #pragma unroll
-  for (uint32_t i = 0; i < kKindGroup; ++i) copy_sub_kind<kPack, kKind>(a, b, mbase, g, q * kKindGroup + i);
+  for (uint32_t i = 0; i < grp; ++i) copy_sub_kind<kPack, kKind, sub>(a, b, mbase, g, q * grp + i);
 }
 
 template <bool kPack>
@@ -150,7 +157,7 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   const bool all = kind_mask == 0xFu;
   const bool single = kind_mask < 16 && (kind_mask & (kind_mask - 1)) == 0;
   if (!all && !single) return hipErrorInvalidValue;  // a launch copies all four kinds or one
-  const uint64_t nwg = uint64_t(ntiles) * (all ? kSubPerTile : kSubPerTile / kKindGroup);
+  const uint64_t nwg = uint64_t(ntiles) * (all ? kSubPerTile : kind_wg_per_tile(kind_mask == 1 ? 2 : 4));
   if (nwg > uint64_t(INT32_MAX)) return hipErrorInvalidValue;
   CopyArgs a{};
   a.boxes = boxes;

@@ -8,7 +8,7 @@
 
 #include <cstdint>
 
-#include "etc_internal.hpp"
+#include "copy_desc.hpp"
 
 namespace etc {
 
@@ -57,14 +57,28 @@ __host__ __device__ inline uint64_t tile_msg_elem(const CopyBox& b, const TileGe
 // elements (one vector per lane at most), else its elements
 // [j * kSubElems, (j + 1) * kSubElems), both in row-major order over the
 // tile and clipped to the tile's size.
-// A launch of one kind gives each workgroup kKindGroup consecutive
-// sub-chunks of one tile instead.
+// A launch of one kind cuts a tile of that kind into kind_sub_elems(es)-element
+// sub-chunks instead and gives each workgroup kind_group(es) consecutive
+// ones of one tile.
 constexpr uint32_t kSubThreads = 64;
 constexpr uint32_t kSubPerTile = 64;
 constexpr uint32_t kSubElems = kTileElems / kSubPerTile;  // 256
-constexpr uint32_t kKindGroup = 8;
-static_assert(kSubPerTile % kKindGroup == 0, "whole groups per tile");
 static_assert(kSubElems / 4 <= kSubThreads, "a 4-byte kind's sub-chunk must fit one vector per lane");
+
+// One-kind launches, for a kind of es bytes per element: elements per
+// sub-chunk (one 16-byte vector per lane of the wavefront: 256 of a 4-byte
+// kind, 512 of bf16), sub-chunks per workgroup (8 KB per workgroup for
+// every kind), and workgroups per tile.
+__host__ __device__ constexpr uint32_t kind_sub_elems(int es) { return kSubThreads * 16u / uint32_t(es); }
+__host__ __device__ constexpr uint32_t kind_group(int /*es*/) { return 8u; }
+__host__ __device__ constexpr uint32_t kind_wg_per_tile(int es) {
+  return kTileElems / kind_sub_elems(es) / kind_group(es);
+}
+static_assert(kTileElems % (kind_sub_elems(2) * kind_group(2)) == 0 &&
+                  kTileElems % (kind_sub_elems(4) * kind_group(4)) == 0,
+              "whole groups per tile");
+static_assert(kind_sub_elems(2) / 8 <= kSubThreads && kind_sub_elems(4) / 4 <= kSubThreads,
+              "a one-kind sub-chunk must fit one vector per lane");
 
 // Whether the kind of element size es moves a tile in 16-byte vectors: the
 // box is vector-aligned for that size and every row of the tile is whole

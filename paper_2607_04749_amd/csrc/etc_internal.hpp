@@ -7,6 +7,7 @@
 #include <string>
 #include <vector>
 
+#include "copy_desc.hpp"
 #include "etc.h"
 
 namespace etc {
@@ -65,30 +66,6 @@ struct RouteTensor {
   int32_t single_copy;   // exactly one copy in both grids
 };
 
-// ---------------------------------------------------------------------------
-// Copy engine descriptors (device)
-// ---------------------------------------------------------------------------
-
-// One routed box between an arena (strided rows) and a message section
-// (contiguous, row-major).  Element offsets are kind-independent; the kernel
-// scales them by each kind's element size.  The message itself is found
-// through the launch's per-peer pointer table.  64 bytes.
-struct CopyBox {
-  uint64_t a_off;     // arena element offset of the box's first element
-  uint64_t m_off;     // element offset inside each kind section of the message
-  uint64_t msg_npad;  // elements per kind section of that message
-  uint64_t m_ld;      // message-side row stride (elements): cols, or a source arena's row stride
-  uint32_t a_ld;      // arena row stride, elements
-  uint32_t rows, cols;  // box shape; contiguous boxes are collapsed to one row
-  uint32_t tr, tc;    // tile shape (rows x cols)
-  uint32_t ntc;       // tiles per row band
-  uint32_t tile0;     // first tile of this box in its launch
-  uint16_t peer;      // peer slot
-  uint8_t pad;        // zero elements after the box in the message (pack)
-  uint8_t vec;        // bit0: 16-byte vectors valid for 2-byte kinds, bit1: for 4-byte kinds
-};
-static_assert(sizeof(CopyBox) == 64, "CopyBox layout");
-
 // Launch table of one rank's pack or unpack.
 struct CopyTable {
   bool built = false;
@@ -99,22 +76,8 @@ struct CopyTable {
   std::vector<int32_t> peers;  // rank of each peer slot (pack: targets, unpack: sources)
 };
 
-constexpr uint32_t kTileElems = 16384;  // nominal tile: 16384 elements per kind
 constexpr int kCmThreads = 256;
 
-// What the message side of a copy launch is.
-enum MsgMode : uint32_t {
-  kMsgOneKind = 0,   // one kind per message (chunk format)
-  kMsgSections = 1,  // four kind sections per message (full format)
-  kMsgArenas = 2,    // no message: peers[k] is a source arena of kind k (Refer)
-};
-
-// kernel launchers (copy.hip, cost.hip)
-// kind_mask: kinds to copy (bit k): all four (one sub-chunk of each kind per
-// workgroup) or one (kKindGroup sub-chunks per workgroup); any other mask is
-// hipErrorInvalidValue, and so is a grid over 2^31 - 1 workgroups
-hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles, uint32_t kind_mask,
-                       MsgMode mode, void* const arena[4], void* const* peers, int npeers, hipStream_t stream);
 // Routing context of a plan: both grids and the failed source ranks (bitmap,
 // nullptr when none).  Device copies point at device memory.
 struct RouteCtx {

@@ -1,7 +1,7 @@
 // tilewalk.cpp -- host replay of the copy kernels' walks over the copy
 // tables the planner builds (pack, unpack and Refer; all kinds at once, one
-// sub-chunk of each kind per workgroup; one kind at a time, kKindGroup
-// sub-chunks per workgroup).  For every tile it checks that each row stays inside its arena,
+// sub-chunk of each kind per workgroup; one kind at a time, kind_group(es)
+// sub-chunks of kind_sub_elems(es) elements per workgroup).  For every tile it checks that each row stays inside its arena,
 // message section or source arena, that vector accesses are 16-byte aligned,
 // that a sub-chunk needs no more lanes than a workgroup has, and that the
 // writes of a launch cover the target bytes exactly once: each message
@@ -60,15 +60,20 @@ static std::vector<Iv> merge_tile(std::vector<Iv> w, const char* what) {
 }
 
 // Replay a launch as the kernels run it: for all four kinds, workgroup
-// t * kSubPerTile + j copies sub-chunk j of every kind of tile t; for one
-// kind, workgroup t * (kSubPerTile / kKindGroup) + q copies its sub-chunks
-// [q * kKindGroup, (q + 1) * kKindGroup) of tile t.  Either way every
-// sub-chunk j of every tile is copied once per kind in the launch.
+// t * kSubPerTile + j copies sub-chunk j (kSubElems elements) of every kind
+// of tile t; for one kind of es bytes, workgroup t * kind_wg_per_tile(es) + q
+// copies its sub-chunks [q * G, (q + 1) * G) of kind_sub_elems(es) elements,
+// G = kind_group(es).  Either way every sub-chunk of every tile is copied
+// once per kind in the launch.
 static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask,
                        uint64_t arena_elems, const std::vector<uint64_t>& peer_bytes,
                        std::vector<std::vector<Iv>> W[4], std::vector<Iv> A[4], bool arenas) {
   const uint32_t nbox = uint32_t(v.size() - 1), ntiles = v.back().tile0;
-  const uint32_t per_tile = kind_mask == 0xFu ? kSubPerTile : kSubPerTile / kKindGroup;
+  const bool all = kind_mask == 0xFu;
+  const int kes = kind_mask == 1u ? 2 : 4;  // element size of a one-kind launch
+  const uint32_t per_tile = all ? kSubPerTile : kind_wg_per_tile(kes);
+  const uint32_t sub_elems = all ? kSubElems : kind_sub_elems(kes);
+  const uint32_t subs_per_tile = kTileElems / sub_elems;
   if (uint64_t(ntiles) * per_tile > uint64_t(INT32_MAX)) { FAIL("grid over 2^31 - 1 workgroups"); return; }
   for (uint32_t t = 0; t < ntiles; ++t) {
     const uint32_t bi = box_of_tile(v.data(), nbox, t);  // the same for every j of the tile
@@ -89,30 +94,33 @@ static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned,
       if (std::max(sp, dp) * (g.nr - 1) + uint64_t(g.nc) * es >= (1ull << 31)) FAIL("tile extent over 2^31");
       const bool vk = sub_vectors(b, g, es);
       const uint32_t unit = vk ? 16u / uint32_t(es) : 1u;  // elements per item
-      const uint32_t per = kSubElems / unit;               // items per sub-chunk
+      const uint32_t per = sub_elems / unit;               // items per sub-chunk
       const uint32_t ipr = g.nc / unit;                    // items per row
       if (vk && per > kSubThreads) FAIL("a vector sub-chunk needs more lanes than threads");
+      if (!all && es != kes) FAIL("one-kind launch of another element size");
       if (vk && g.nc % unit) FAIL("vector rows not whole vectors");
       std::vector<Iv> tw;
       // the sub-chunks of tile t, in the order and with the index arithmetic
       // of the kernels' workgroups
       std::vector<uint32_t> subs;
       for (uint32_t w = t * per_tile; w < (t + 1) * per_tile; ++w) {
-        if (kind_mask == 0xFu) {
+        if (all) {
           if (w / kSubPerTile != t) FAIL("workgroup %u maps to another tile", w);
           subs.push_back(w % kSubPerTile);
         } else {
-          constexpr uint32_t groups = kSubPerTile / kKindGroup;
+          const uint32_t groups = kind_wg_per_tile(kes), grp = kind_group(kes);
           if (w / groups != t) FAIL("workgroup %u maps to another tile", w);
-          for (uint32_t i = 0; i < kKindGroup; ++i) subs.push_back((w % groups) * kKindGroup + i);
+          for (uint32_t i = 0; i < grp; ++i) subs.push_back((w % groups) * grp + i);
         }
       }
-      std::vector<char> seen(kSubPerTile, 0);
+      std::vector<char> seen(subs_per_tile, 0);
       for (uint32_t j : subs) {
-        if (j >= kSubPerTile || seen[j]++) FAIL("sub-chunk %u of tile %u copied twice or out of range", j, t);
+        if (j >= subs_per_tile || seen[j]++) FAIL("sub-chunk %u of tile %u copied twice or out of range", j, t);
       }
+      if (subs.size() != subs_per_tile) FAIL("tile %u: %zu sub-chunks copied, %u in the tile", t, subs.size(),
+                                             subs_per_tile);
       for (uint32_t j : subs) {
-        if (j >= kSubPerTile) continue;
+        if (j >= subs_per_tile) continue;
         uint32_t lo, hi;
         sub_range(j, per, g.nr * ipr, &lo, &hi);
         for (uint32_t r = lo / (ipr ? ipr : 1); lo < hi && r <= (hi - 1) / ipr; ++r) {
