@@ -63,15 +63,22 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, kernel, algorithmic):
-    """HBM bytes per launch from committed rocprofv3 PMC counters, or None when
-    absent or taken on a different version of the copy kernel."""
+def launch_key(mode, side, kind):
+    """Name of a kind of copy launch in the traffic record: mode/side, plus
+    /kindK for a one-kind launch."""
+    return f"{mode}/{side}" + ("" if kind is None else f"/kind{kind}")
+
+
+def measured_traffic(workload, key):
+    """HBM bytes per launch from committed rocprofv3 PMC counters for the
+    launch `key` (launch_key) of the sketch-paired share, or None when absent
+    or taken on a different version of the copy kernel."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    ent = rec.get(workload, {}).get(kernel)
+    ent = rec.get(workload, {}).get(key)
     if not ent or ent.get("kernel_hash") != kernel_hash():
         return None
     return ent.get("bytes_per_launch")
@@ -320,6 +327,8 @@ def run_share(w, args):
         f"{sum(x.numel() for v in dst.values() for x in v) / 1e9:.1f} GB targets, "
         f"{stage_bytes / 1e9:.1f} GB message buffers")
 
+    # one step's copy launches in order (the counter records map dispatches to them)
+    log("step launches: " + json.dumps([[l[0], l[1], l[2], l[4]] for l in launches]))
     pack_bytes = sum(l[4] for l in launches if l[0] == "pack")
     unpack_bytes = sum(l[4] for l in launches if l[0] == "unpack")
     refer_bytes = sum(l[4] for l in launches if l[0] == "refer")
@@ -335,6 +344,11 @@ def run_share(w, args):
         if ev:
             ev[-1].record(stream)
 
+    # no cyclic garbage collection while launches are queued: a full pass
+    # can stall the host for tens of milliseconds, longer than the queue of
+    # a step made of many short launches (the 1.3B chunked step)
+    gc.collect()
+    gc.disable()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -346,6 +360,7 @@ def run_share(w, args):
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gc.enable()
     ms_per_step = wall * 1e3 / args.steps
     launch_ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
                  for i in range(len(launches))]
@@ -397,8 +412,7 @@ def run_share(w, args):
         g[2] += 1
     (side, kind), (g_ms, g_bytes, g_n) = max(groups.items(), key=lambda kv: kv[1][0])
     achieved = (g_bytes / g_n) / ((g_ms / g_n) * 1e-3) / 1e9
-    traffic = measured_traffic(w.name, side, g_bytes / g_n) if args.mode == "direct" and \
-        not args.identity else None
+    traffic = None if args.identity else measured_traffic(w.name, launch_key(args.mode, side, kind))
     # all four kinds run as copy_sub_kernel, one kind as copy_kind_kernel
     kernel = f"copy_sub_kernel ({side})" if kind is None else f"copy_kind_kernel ({side}, kind {kind})"
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
@@ -429,6 +443,11 @@ def run_share(w, args):
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic},
     }
+    if args.mode == "chunked":  # each state kind's launches
+        out["kinds"] = {str(k): {f"{sd}_GBps": rate(sum(l[4] for l in launches if l[:2] == (sd, k)),
+                                                    sum(t for t, l in zip(launch_ms, launches)
+                                                        if l[:2] == (sd, k)))
+                                 for sd in ("pack", "unpack")} for k in range(4)}
     if args.mode == "refer":
         out["refer_GBps"] = rate(refer_bytes, refer_ms)
         out["refer_ms"] = round(refer_ms, 4)

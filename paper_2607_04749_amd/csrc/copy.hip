@@ -13,7 +13,8 @@
 // every kind, copied kind after kind; a launch of one kind (state chunking)
 // gives each workgroup kind_group consecutive sub-chunks of that kind, each a
 // full wavefront of vectors (kind_sub_elems: 1 KB, 512 bf16 elements or 256
-// fp32 ones), 8 KB per workgroup.
+// fp32 ones), 8 KB per workgroup, and walks the tiles in one window per XCD
+// at a time (kind_wg_tile).
 // Either way a workgroup finds its tile's descriptor once (a binary search of
 // the tile table, scalar loads) and then moves a few KB.  The hardware
 // dispatches the workgroups in index order, so the whole GPU advances
@@ -128,8 +129,9 @@ __global__ __launch_bounds__(kSubThreads) void copy_sub_kernel(CopyArgs a) {
 template <bool kPack, int kKind>
 __device__ __forceinline__ void copy_kind_group(const CopyArgs& a) {
   constexpr int es = kKind == 0 ? 2 : 4;
-  constexpr uint32_t sub = kind_sub_elems(es), grp = kind_group(es), groups = kind_wg_per_tile(es);
-  const uint32_t t = blockIdx.x / groups, q = blockIdx.x % groups;
+  constexpr uint32_t sub = kind_sub_elems(es), grp = kind_group(es);
+  uint32_t t, q;
+  if (!kind_wg_tile(blockIdx.x, a.ntiles, es, &t, &q)) return;  // past the last tile
   const uint32_t bi = box_of_tile(a.boxes, a.nbox, t);
   const CopyBox b = a.boxes[bi];
   const TileGeom g = tile_geom(b, t, a.boxes[bi + 1].tile0);
@@ -157,7 +159,7 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   const bool all = kind_mask == 0xFu;
   const bool single = kind_mask < 16 && (kind_mask & (kind_mask - 1)) == 0;
   if (!all && !single) return hipErrorInvalidValue;  // a launch copies all four kinds or one
-  const uint64_t nwg = uint64_t(ntiles) * (all ? kSubPerTile : kind_wg_per_tile(kind_mask == 1 ? 2 : 4));
+  const uint64_t nwg = all ? uint64_t(ntiles) * kSubPerTile : kind_grid(ntiles, kind_mask == 1 ? 2 : 4);
   if (nwg > uint64_t(INT32_MAX)) return hipErrorInvalidValue;
   CopyArgs a{};
   a.boxes = boxes;

@@ -80,6 +80,35 @@ static_assert(kTileElems % (kind_sub_elems(2) * kind_group(2)) == 0 &&
 static_assert(kind_sub_elems(2) / 8 <= kSubThreads && kind_sub_elems(4) / 4 <= kSubThreads,
               "a one-kind sub-chunk must fit one vector per lane");
 
+// The workgroups of a one-kind launch walk the tile list in windows, one
+// per XCD at a time: the list is cut into kXcds * kKindWindows equal windows
+// of consecutive tiles, and the workgroups of XCD x (the hardware deals
+// workgroup w to XCD w % kXcds) copy window x, then window x + kXcds, ...,
+// each in tile order.  A launch of one kind has one read and one write
+// stream; eight fronts far apart in each, every one fed by one XCD, kept
+// them faster than one compact front on MI355X (the all-kinds launches,
+// with four streams each way, stay compact).  Two windows per XCD rather
+// than one keep the XCDs' shares of strided and contiguous tiles even.
+constexpr uint32_t kXcds = 8;
+constexpr uint32_t kKindWindows = 2;
+__host__ __device__ inline uint32_t kind_window_tiles(uint32_t ntiles) {
+  return (ntiles + kXcds * kKindWindows - 1) / (kXcds * kKindWindows);
+}
+// workgroups in a one-kind launch over ntiles tiles (a few past the last
+// tile, when the windows overhang it, find no tile)
+__host__ __device__ inline uint64_t kind_grid(uint32_t ntiles, int es) {
+  return uint64_t(kXcds) * kKindWindows * kind_window_tiles(ntiles) * kind_wg_per_tile(es);
+}
+// Tile t and group q (sub-chunks [q * kind_group, (q + 1) * kind_group)) of
+// workgroup w of a one-kind launch; false for a workgroup past the last tile.
+__host__ __device__ inline bool kind_wg_tile(uint32_t w, uint32_t ntiles, int es, uint32_t* t, uint32_t* q) {
+  const uint32_t gpt = kind_wg_per_tile(es), per = kind_window_tiles(ntiles);
+  const uint32_t x = w % kXcds, k = w / kXcds, s = k / gpt, m = s / per;
+  *t = (m * kXcds + x) * per + s % per;
+  *q = k % gpt;
+  return m < kKindWindows && *t < ntiles;
+}
+
 // Whether the kind of element size es moves a tile in 16-byte vectors: the
 // box is vector-aligned for that size and every row of the tile is whole
 // vectors (a ragged single-row tile goes element by element).

@@ -23,18 +23,29 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_traffic_record_matches_the_kernel():
-    """Every record in the committed traffic file carries the hash of the
-    current copy-kernel sources, so bench.py reports it (a kernel change
-    without new counters would make it null)."""
+    """The committed traffic record covers every launch shape bench.py times
+    (each mode of the 70B and 7B shares, and the 13B and 1.3B workloads),
+    every entry carries the hash of the current copy-kernel sources, so
+    bench.py reports it (a kernel change without new counters would make it
+    null), and measured traffic is within 1 % of the algorithmic bytes."""
     with open(bench.TRAFFIC_FILE) as f:
         rec = json.load(f)
-    assert set(rec) >= {"llama-70b", "llama-7b"}
-    for wl, kernels in rec.items():
-        for side, ent in kernels.items():
-            assert ent["kernel_hash"] == bench.kernel_hash(), (wl, side)
-            assert bench.measured_traffic(wl, side, 0) == ent["bytes_per_launch"]
+    kinds = {bench.launch_key("chunked", side, k) for side in ("pack", "unpack") for k in range(4)}
+    need = {
+        "llama-70b": {"direct/pack", "direct/unpack", "refer/refer", "refer/unpack", "coalesced/pack",
+                      "coalesced/unpack"} | kinds,
+        "llama-7b": {"direct/pack", "direct/unpack", "refer/refer", "refer/unpack"} | kinds,
+        "llama-13b": {"direct/pack", "direct/unpack", "refer/refer", "refer/pack"} | kinds,
+        "gpt-1.3b": {"direct/pack", "direct/unpack"} | kinds,
+    }
+    for wl, keys in need.items():
+        assert keys <= set(rec[wl]), (wl, keys - set(rec[wl]))
+    for wl, launches in rec.items():
+        for key, ent in launches.items():
+            assert ent["kernel_hash"] == bench.kernel_hash(), (wl, key)
+            assert bench.measured_traffic(wl, key) == ent["bytes_per_launch"]
             # within 1 % of the algorithmic bytes: nothing is fetched twice
-            assert abs(ent["bytes_per_launch"] / ent["algorithmic_bytes"] - 1) < 0.01, (wl, side)
+            assert abs(ent["bytes_per_launch"] / ent["algorithmic_bytes"] - 1) < 0.01, (wl, key)
 
 
 @pytest.mark.parametrize("pairing", ["identity", "sketch"])

@@ -61,19 +61,34 @@ static std::vector<Iv> merge_tile(std::vector<Iv> w, const char* what) {
 
 // Replay a launch as the kernels run it: for all four kinds, workgroup
 // t * kSubPerTile + j copies sub-chunk j (kSubElems elements) of every kind
-// of tile t; for one kind of es bytes, workgroup t * kind_wg_per_tile(es) + q
-// copies its sub-chunks [q * G, (q + 1) * G) of kind_sub_elems(es) elements,
-// G = kind_group(es).  Either way every sub-chunk of every tile is copied
-// once per kind in the launch.
+// of tile t; for one kind of es bytes, workgroup w of kind_grid(ntiles, es)
+// copies, when kind_wg_tile(w) gives it tile t and group q, its sub-chunks
+// [q * G, (q + 1) * G) of kind_sub_elems(es) elements, G = kind_group(es).
+// Either way every sub-chunk of every tile must be copied once per kind in
+// the launch.
 static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned, uint32_t kind_mask,
                        uint64_t arena_elems, const std::vector<uint64_t>& peer_bytes,
                        std::vector<std::vector<Iv>> W[4], std::vector<Iv> A[4], bool arenas) {
   const uint32_t nbox = uint32_t(v.size() - 1), ntiles = v.back().tile0;
   const bool all = kind_mask == 0xFu;
   const int kes = kind_mask == 1u ? 2 : 4;  // element size of a one-kind launch
-  const uint32_t per_tile = all ? kSubPerTile : kind_wg_per_tile(kes);
+  const uint32_t per_tile = kSubPerTile;  // all-kinds launches
   const uint32_t sub_elems = all ? kSubElems : kind_sub_elems(kes);
   const uint32_t subs_per_tile = kTileElems / sub_elems;
+  // one-kind launches: the groups each tile receives, from the whole grid
+  std::vector<std::vector<uint32_t>> groups_of;
+  if (!all) {
+    const uint64_t grid = kind_grid(ntiles, kes);
+    if (grid > uint64_t(INT32_MAX)) { FAIL("grid over 2^31 - 1 workgroups"); return; }
+    if (grid < uint64_t(ntiles) * kind_wg_per_tile(kes)) FAIL("one-kind grid smaller than the work");
+    groups_of.resize(ntiles);
+    for (uint64_t w = 0; w < grid; ++w) {
+      uint32_t t, q;
+      if (!kind_wg_tile(uint32_t(w), ntiles, kes, &t, &q)) continue;  // coverage below catches a wrong refusal
+      if (t >= ntiles || q >= kind_wg_per_tile(kes)) { FAIL("workgroup %llu maps outside", (unsigned long long)w); continue; }
+      groups_of[t].push_back(q);
+    }
+  }
   if (uint64_t(ntiles) * per_tile > uint64_t(INT32_MAX)) { FAIL("grid over 2^31 - 1 workgroups"); return; }
   for (uint32_t t = 0; t < ntiles; ++t) {
     const uint32_t bi = box_of_tile(v.data(), nbox, t);  // the same for every j of the tile
@@ -103,15 +118,15 @@ static void replay_sub(const std::vector<CopyBox>& v, bool pack, bool sectioned,
       // the sub-chunks of tile t, in the order and with the index arithmetic
       // of the kernels' workgroups
       std::vector<uint32_t> subs;
-      for (uint32_t w = t * per_tile; w < (t + 1) * per_tile; ++w) {
-        if (all) {
+      if (all) {
+        for (uint32_t w = t * per_tile; w < (t + 1) * per_tile; ++w) {
           if (w / kSubPerTile != t) FAIL("workgroup %u maps to another tile", w);
           subs.push_back(w % kSubPerTile);
-        } else {
-          const uint32_t groups = kind_wg_per_tile(kes), grp = kind_group(kes);
-          if (w / groups != t) FAIL("workgroup %u maps to another tile", w);
-          for (uint32_t i = 0; i < grp; ++i) subs.push_back((w % groups) * grp + i);
         }
+      } else {
+        const uint32_t grp = kind_group(kes);
+        for (uint32_t q : groups_of[t])
+          for (uint32_t i = 0; i < grp; ++i) subs.push_back(q * grp + i);
       }
       std::vector<char> seen(subs_per_tile, 0);
       for (uint32_t j : subs) {
