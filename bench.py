@@ -11,10 +11,11 @@ and the new rank it becomes.
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
                     [--identity] [--mode direct|chunked|coalesced|refer]
 
-With no --workload the run times the Llama-70B share (the line's value and
-roofline) and then, after freeing its buffers, the Llama-7B share, reported
-under "shares" with its own rate, roofline and CPU baseline: the two shares
-the 70 % target is stated on.  --workload NAME times that workload alone.
+With no --workload the run times the Llama-70B share (the line's value,
+roofline and CPU baseline) and then the Llama-7B share (under "shares", with
+its own rate, roofline and CPU baseline), each in a process of its own, as a
+deployment runs one migration per process: the two shares the 70 % target is
+stated on.  --workload NAME times that workload alone, in this process.
 
 Modes: direct (default) packs and unpacks all four state kinds in one launch
 each; chunked moves one state kind at a time through per-kind chunk buffers
@@ -39,6 +40,7 @@ import gc
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -472,33 +474,42 @@ def main():
         print("--identity and --mode coalesced exclude each other", file=sys.stderr)
         sys.exit(2)
 
+    if not args.workload:
+        # Both gated shares, each in a process of its own (one migration per
+        # process, as deployed), the 70B share first; this process makes no
+        # GPU call, so none forks with GPU state.
+        outs = {}
+        for name in ("llama-70b", "llama-7b"):
+            cmd = [sys.executable, os.path.abspath(__file__), "--workload", name, "--steps",
+                   str(args.steps), "--warmup", str(args.warmup), "--mode", args.mode]
+            cmd += ["--no-cpu-baseline"] * args.no_cpu_baseline + ["--identity"] * args.identity
+            log(f"{name}: timed in a process of its own")
+            r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+            if r.returncode != 0:
+                print(f"the {name} share failed (exit {r.returncode})", file=sys.stderr)
+                sys.exit(r.returncode)
+            outs[name] = json.loads([x for x in r.stdout.splitlines() if x.startswith("{")][-1])
+        line, out = outs["llama-70b"], outs["llama-7b"]
+        line["shares"] = {"llama-7b": {"workload": out["config"]["workload"],
+                                       "alg_bytes_per_step": out["config"]["alg_bytes_per_step"],
+                                       **{k: out[k] for k in SHARE_KEYS + ("cpu_baseline",) if k in out}}}
+        print(json.dumps(line), flush=True)
+        return
+
     import torch
 
     from paper_2607_04749_amd.workloads import WORKLOADS
 
     torch.cuda.set_device(0)
-    names = [args.workload] if args.workload else ["llama-70b", "llama-7b"]
-    line, shares = None, {}
-    for name in names:
-        w = WORKLOADS[name]
-        out, pairing = run_share(w, args)
-        gc.collect()  # the share's buffers go before the next share allocates its own
-        torch.cuda.synchronize()
-        torch.cuda.empty_cache()
-        if not args.no_cpu_baseline:
-            log(f"{name}: cpu baseline (oracle) ...")
-            out["cpu_baseline"] = cpu_baseline(w, pairing, direct_refer=args.mode == "refer")
-        if line is None:
-            line = out
-        else:
-            shares[name] = {"workload": out["config"]["workload"],
-                            "alg_bytes_per_step": out["config"]["alg_bytes_per_step"],
-                            **{k: out[k] for k in SHARE_KEYS + ("cpu_baseline",) if k in out}}
-    if shares:
-        line["shares"] = shares
+    w = WORKLOADS[args.workload]
+    line, pairing = run_share(w, args)
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log(f"{w.name}: cpu baseline (oracle) ...")
+        line["cpu_baseline"] = cpu_baseline(w, pairing, direct_refer=args.mode == "refer")
     print(json.dumps(line), flush=True)
-
-
 
 
 if __name__ == "__main__":
