@@ -137,3 +137,33 @@ def test_contiguous_run_beyond_2_32_elements(tilewalk):
         for refer in (False, True):
             jobs.append(_args(m, P(1, 1), b, refer, "identity"))
     _run_all(tilewalk, jobs)
+
+
+PLANTS = {
+    # one-kind windows rounded down: the last tiles of a launch get no workgroup
+    "windows rounded down": ("return (ntiles + kXcds * kKindWindows - 1) / (kXcds * kKindWindows);",
+                             "return ntiles / (kXcds * kKindWindows) + (ntiles < kXcds * kKindWindows);"),
+    # a sub-chunk one item short: the last vector or element of each sub-chunk is never copied
+    "sub-chunk one item short": ("*hi = a + per < n ? a + per : n;", "*hi = a + per - 1 < n ? a + per - 1 : n;"),
+}
+
+
+@pytest.mark.parametrize("plant", sorted(PLANTS))
+def test_replay_catches_a_planted_geometry_mistake(tmp_path, plant):
+    """The replay is built against a copy of the kernels' geometry header with
+    one mistake planted; it must then fail on Tiny GPT under either pairing,
+    with and without direct Refer."""
+    old, new = PLANTS[plant]
+    src = open(os.path.join(CSRC, "copy_geom.hpp")).read()
+    assert src.count(old) == 1
+    (tmp_path / "copy_geom.hpp").write_text(src.replace(old, new))
+    exe = str(tmp_path / "tilewalk")
+    subprocess.run(["hipcc", "-x", "hip", "-O2", "-std=c++17", "--offload-arch=gfx950",
+                    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                    "-I", str(tmp_path), "-I", os.path.join(ROOT, "include"), "-I", CSRC, SRC,
+                    *[os.path.join(CSRC, x) for x in LIB_SOURCES], "-o", exe],
+                   check=True, capture_output=True)
+    w = WORKLOADS["tiny-gpt"]
+    for args in (_args(w.model, w.src, w.dst, False, "identity"), _args(w.model, w.src, w.dst, True, "sketch")):
+        r = subprocess.run([exe, *args], capture_output=True, text=True, timeout=600)
+        assert r.returncode != 0 and r.stdout.strip() != "ok", (plant, " ".join(args))
