@@ -163,12 +163,12 @@ def _buf(x, need, what):
     return x.data_ptr()
 
 
-def _arenas(plan, side, rank, arenas, what, kinds=range(4)):
+def _arenas(plan, side, rank, arenas, what):
+    """Pointers of a rank's four arenas, each checked as _buf does."""
     if len(arenas) != 4:
         raise ValueError(f"{what} needs 4 arenas, got {len(arenas)}")
     e = plan.arena_elems(side, rank)
-    return [_buf(arenas[k], e * ESIZE[k], f"{what}[{k}]") if k in kinds else _ptr(arenas[k])
-            for k in range(4)]
+    return [_buf(arenas[k], e * ESIZE[k], f"{what}[{k}]") for k in range(4)]
 
 
 def last_error():

@@ -1,7 +1,7 @@
 """GPU test helpers: device arenas filled with the seeded states at the
 oracle's layout, chunked bitwise comparison, whole send buffers expected
-from the oracle's message boxes, windows of the oracle's own migration at
-real shape, and sampled gathers."""
+from the oracle's message boxes, the oracle's own migration of a whole
+share at real shape, and sampled gathers."""
 from __future__ import annotations
 
 import sys
@@ -244,98 +244,39 @@ def check_chunks(plan, model, src, dst, s, k, chunk, exp_send):
     assert equal(chunk[:exp.numel()], exp), f"chunk buffer of source {s} kind {k}"
 
 
-def share_windows(model, src, dst, s0, d0, pair=None):
-    """Three contiguous windows of tensor ids that a share touches (tensors
-    of target d0's pieces or of source s0's messages): the first touched
-    tensor (the embedding when the share holds stage 0), the tensors of the
-    middle layer that s0's messages carry (of the target's layers if they
-    carry none), and those of the target's last layer together with every
-    touched tensor after it (final norm and head)."""
-    T = oracle.tensors(model)
-    held = {p["tensor"] for p in oracle.layout(model, dst, d0)[0]}
-    sent = set()
-    cnt = oracle.send_layout(model, src, dst, s0, pair=pair)[0]
-    for d in np.nonzero(cnt)[0]:
-        sent |= {b["tensor"] for b in oracle.message(model, src, dst, s0, int(d), pair=pair)[0]}
-    touched = held | sent
-
-    def layers(ids):
-        return sorted({T[t]["layer"] for t in ids if T[t]["layer"] >= 0})
-
-    def span(ly):
-        ids = [t for t in range(len(T)) if T[t]["layer"] == ly]
-        return min(ids), max(ids) + 1
-
-    first = min(touched)
-    out = [(first, first + 1)]
-    mid = layers(sent) or layers(held)
-    lo, hi = span(mid[len(mid) // 2])
-    if lo >= out[-1][1]:
-        out.append((lo, hi))
-    lo, hi = span(layers(held)[-1])
-    hi = max(max(touched) + 1, hi)
-    if lo >= out[-1][1]:
-        out.append((lo, hi))
-    return out
+def oracle_whole_check(model, src, dst, pair, dev_src, packed, d0, dev_send, dev_dst, threads=16):
+    """The oracle's own migration of a whole share at real shape, against the
+    GPU's: the resident sources (from the seeded generator, copied from the
+    device) are materialized and cut one logical tensor per thread (the
+    oracle's calls write disjoint bytes), into fresh host arenas for target
+    d0 and send buffers for the packed sources; then every byte of d0's
+    arenas and of those send buffers must equal the GPU's."""
+    from concurrent.futures import ThreadPoolExecutor
+    hs = {s: [x.cpu().numpy() for x in ar] for s, ar in dev_src.items()}
+    hd = [np.zeros(x.numel(), np.uint8) for x in dev_dst]
+    hb = {s: np.zeros(max(oracle.send_layout(model, src, dst, s, pair=pair)[3], 1), np.uint8)
+          for s in packed}
+    nt = len(oracle.tensors(model))
+    say(f"  the oracle: {nt} tensors on {threads} threads")
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(lambda t: oracle.migrate(model, src, dst, hs, {d0: hd}, hb, t, t + 1, pair=pair),
+                    range(nt)))
+    del hs
+    for k in range(4):
+        assert equal(dev_dst[k], torch.from_numpy(hd[k]).to(DEV)), f"target {d0} kind {k} vs the oracle"
+    for s in packed:
+        n = dev_send[s].numel()
+        assert equal(dev_send[s], torch.from_numpy(hb[s][:n]).to(DEV)), f"send buffer {s} vs the oracle"
+    say(f"  {sum(x.numel() for x in dev_dst) / 1e9:.1f} GB of target and "
+        f"{sum(dev_send[s].numel() for s in packed) / 1e9:.1f} GB of messages equal to the oracle's")
 
 
-def oracle_window_check(model, src, dst, seed, pair, resident, packed, d0, dev_send, dev_dst,
-                        windows, direct_refer=False):
-    """The oracle's own migration over windows of tensor ids, at real shape:
-    fresh lazily zeroed host arenas, the resident sources' pieces in the
-    window filled with the seeded values, materialize-then-cut for target d0
-    and the packed sources' messages; then the GPU's target pieces and
-    message boxes of those tensors byte for byte against it."""
-    fc = full_cols(model)
-    dl = oracle.layout(model, dst, d0)
-    for t_lo, t_hi in windows:
-        say(f"  oracle window: tensors [{t_lo}, {t_hi})")
-        hs = {}
-        for s in resident:
-            pieces, elems = oracle.layout(model, src, s)
-            hs[s] = [np.zeros(elems * e, np.uint8) for e in ESIZE]
-            synth.fill_host([p for p in pieces if t_lo <= p["tensor"] < t_hi], fc, hs[s], seed)
-        hd = [np.zeros(dl[1] * e, np.uint8) for e in ESIZE]
-        hb = {s: np.zeros(max(oracle.send_layout(model, src, dst, s, pair=pair,
-                                                 direct_refer=direct_refer)[3], 1), np.uint8)
-              for s in packed}
-        oracle.migrate(model, src, dst, hs, {d0: hd}, hb, t_lo, t_hi, pair=pair,
-                       direct_refer=direct_refer)
-        nb = 0
-        for p in dl[0]:
-            if not t_lo <= p["tensor"] < t_hi:
-                continue
-            n = (p["r1"] - p["r0"]) * (p["c1"] - p["c0"])
-            for k in range(4):
-                a, b = p["off"] * ESIZE[k], (p["off"] + n) * ESIZE[k]
-                assert np.array_equal(dev_dst[k][a:b].cpu().numpy(), hd[k][a:b]), \
-                    f"target {d0} tensor {p['tensor']} kind {k} vs the oracle"
-                nb += b - a
-        for s in packed:
-            cnt, mb, dsp, _ = oracle.send_layout(model, src, dst, s, pair=pair, direct_refer=direct_refer)
-            for d in np.nonzero(mb)[0]:
-                boxes, npad = oracle.message(model, src, dst, s, int(d), pair=pair,
-                                             direct_refer=direct_refer)
-                for x in boxes:
-                    if not t_lo <= x["tensor"] < t_hi:
-                        continue
-                    n = (x["r1"] - x["r0"]) * (x["c1"] - x["c0"])
-                    for k in range(4):
-                        a = int(dsp[d]) + npad * SECTION[k] + x["moff"] * ESIZE[k]
-                        b = a + n * ESIZE[k]
-                        assert np.array_equal(dev_send[s][a:b].cpu().numpy(), hb[s][a:b]), \
-                            f"message {s}->{d} tensor {x['tensor']} kind {k} vs the oracle"
-                        nb += b - a
-        say(f"    {nb / 1e9:.2f} GB equal to the oracle's")
-        del hs, hd, hb
-
-
-def share_run(w, plan, pair=None, check=True, windows=False):
+def share_run(w, plan, pair=None, check=True, whole=False):
     """Pack the share's source (and the sources feeding its target), unpack the
     target; check every packed send buffer in full (expected from the
-    oracle's message boxes), with windows also three windows of tensors
-    against the oracle's own migration, sampled origins, and the whole
-    target against the seeded values."""
+    oracle's message boxes), with whole also the whole share against the
+    oracle's own migration, sampled origins, and the whole target against
+    the seeded values."""
     s0 = w.pack_rank
     d0 = plan.process(w.unpack_rank)[1] if pair is not None else w.unpack_rank
     feeders = [int(s) for s in np.nonzero(plan.recv_counts(d0))[0]]
@@ -358,9 +299,9 @@ def share_run(w, plan, pair=None, check=True, windows=False):
             n = check_send(plan, w.model, w.src, w.dst, s, send[s], w.seed, pair=pair)
             say(f"  send buffer of source {s}: {n} messages, {send[s].numel() / 1e9:.2f} GB, every byte")
             torch.cuda.empty_cache()
-        if windows:
-            oracle_window_check(w.model, w.src, w.dst, w.seed, pair, resident, [s0], d0, send, dd,
-                                share_windows(w.model, w.src, w.dst, s0, d0, pair=pair))
+        if whole:
+            oracle_whole_check(w.model, w.src, w.dst, pair, ds, [s0], d0, send, dd)
+            torch.cuda.empty_cache()
         say("  sampled origins of target", d0)
         sampled_origin_check(w.model, w.src, w.dst, d0, dd, ds, pair=pair)
     del send

@@ -4,9 +4,10 @@ Small workloads (micro models, Tiny GPT) are compared byte for byte over
 every message and every target arena.  At full size every byte of every
 send buffer a test packs is compared with the oracle's message boxes filled
 with the seeded values, every target byte with the seeded values (an
-independent closed form), windows of tensors with the oracle's own
-migration run at real shape, and sampled elements with the oracle's
-per-element origins; plus round trips and identity configurations."""
+independent closed form), the whole migration or share against the
+oracle's own migration run at real shape, and sampled elements with the
+oracle's per-element origins; plus round trips and identity
+configurations."""
 import numpy as np
 import pytest
 import torch
@@ -106,6 +107,38 @@ def test_gpt_1_3b_full_emulation(pairing):
             assert equal(back[s][k], ds[s][k]), f"round trip source {s} kind {k}"
 
 
+def test_gpt_1_3b_whole_migration_against_the_oracle():
+    """The whole GPT-1.3B 8 -> 8 migration (sketch pairing) against the
+    oracle's own migration of the same states at real shape: every byte of
+    every send buffer and every target arena.  The sources come from the
+    seeded generator (on the device, then copied to the host); the oracle
+    runs one logical tensor per thread (its calls write disjoint bytes)."""
+    from concurrent.futures import ThreadPoolExecutor
+    w = WORKLOADS["gpt-1.3b"]
+    m, a, b = w.model, w.src, w.dst
+    pr = oracle_sketch(w)
+    plan = etc.etc_plan(m, a, b, pair=pr)
+    ds = seeded_arenas(m, a, range(a.world), w.seed)
+    say("gpt-1.3b whole migration: GPU pack and unpack of every rank")
+    send, dd = emulate(plan, ds, range(b.world), lambda d: alloc(plan.arena_elems(etc.SIDE_DST, d)))
+    hs = {s: [x.cpu().numpy() for x in ds[s]] for s in ds}
+    del ds
+    torch.cuda.empty_cache()
+    hd = {d: [np.zeros(x.numel(), np.uint8) for x in dd[d]] for d in dd}
+    hb = {s: np.zeros(oracle.send_layout(m, a, b, s, pair=pr)[3], np.uint8) for s in range(a.world)}
+    nt = len(oracle.tensors(m))
+    say(f"  the oracle: materialize and cut {nt} tensors on 16 threads")
+    with ThreadPoolExecutor(16) as ex:
+        list(ex.map(lambda t: oracle.migrate(m, a, b, hs, hd, hb, t, t + 1, pair=pr), range(nt)))
+    del hs
+    say("  every send buffer and target byte against the oracle's")
+    for s in range(a.world):
+        assert equal(send[s], torch.from_numpy(hb[s]).to(send[s].device)), f"send buffer of source {s}"
+    for d in range(b.world):
+        for k in range(4):
+            assert equal(dd[d][k], torch.from_numpy(hd[d][k]).to(dd[d][k].device)), f"target {d} kind {k}"
+
+
 @pytest.mark.parametrize("pairing", ["identity", "sketch"])
 @pytest.mark.parametrize("wl", ["llama-7b", "llama-13b", "llama-70b"])
 def test_share_at_full_size(wl, pairing):
@@ -114,15 +147,15 @@ def test_share_at_full_size(wl, pairing):
     (for these workloads the library's own sketch finds the same pairing).
     Every send buffer packed is compared in full: the 13B source 0 packs
     messages to targets 0 and 1, and under the identity pairing also the
-    norms message to target 4.  The oracle's own migration checks three
-    windows of tensors in the benchmark's configuration, and under the
-    identity pairing at 13B."""
+    norms message to target 4.  The oracle's own migration of the whole
+    share checks every target and message byte in the benchmark's
+    configuration, and under the identity pairing at 13B."""
     w = WORKLOADS[wl]
     pr = oracle_sketch(w) if pairing == "sketch" else None
     say(wl, "share", w.src, "->", w.dst, pairing, "process", w.pack_rank)
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr)
     check_matrices(plan, w.model, w.src, w.dst, pr)
-    share_run(w, plan, pair=pr, windows=pairing == "sketch" or wl == "llama-13b")
+    share_run(w, plan, pair=pr, whole=pairing == "sketch" or wl == "llama-13b")
 
 
 def test_max_peers_full_emulation():
