@@ -4,7 +4,8 @@ the second on a smaller input, each through the C ABI: every device call
 made with the static plan (cost matrices, pack, unpack, Refer, one-kind pack
 and unpack) gives the same bytes as with etc_plan's plan, and the first
 static plan's device calls are refused once the second has replaced its
-tables."""
+tables, and that a plan whose tables exceed the array is refused without
+disturbing the live one."""
 import pytest
 import torch
 
@@ -92,4 +93,16 @@ def test_static_plan_twice_matches_plan():
             p_plan.free()
         prev = (st, src)
         ref.free()
+    torch.cuda.synchronize()
+    # tables over the limit (Llama-70B at DP 8, every rank: about 4.9 MB) are
+    # refused before anything is written, and the live static plan still works
+    w70 = WORKLOADS["llama-70b"]
+    say("static plan over ETC_STATIC_TABLE_BYTES: llama-70b DP8, every rank")
+    with pytest.raises(etc.EtcError) as e:
+        etc.etc_plan_static(w70.model, Parallel(8, 8, 8), Parallel(8, 4, 8))
+    assert e.value.code == etc.ERR_UNSUPPORTED and "ETC_STATIC_TABLE_BYTES" in str(e.value)
+    st, src = prev
+    model, a, b, seed = MICRO_MODELS["llama_gqa"], Parallel(2, 2), Parallel(4, 1), 97
+    ref = etc.etc_plan(model, a, b)
+    _same_results(ref, st, model, a, b, seed)
     torch.cuda.synchronize()
