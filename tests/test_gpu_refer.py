@@ -2,14 +2,15 @@
 holds stays on that GPU): with ETC_PLAN_DIRECT_REFER the kept part is copied
 arena to arena by etc_refer and the paired source's message is empty.
 Targets and every message byte against the oracle under the same switch;
-the 70B share at real shape against the seeded values."""
+the 70B, 7B and 13B shares at real shape against the oracle's own migration
+of the whole share and against the seeded values."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_util import (DEV, alloc, check_send, equal, expected_dst, full_compare, sampled_origin_check, say,
-                      seeded_arenas)
+from gpu_util import (DEV, alloc, check_send, equal, expected_dst, full_compare, oracle_whole_check,
+                      sampled_origin_check, say, seeded_arenas)
 from micro import MICRO_MODELS, cfg_pairs
 from paper_2607_04749_amd import etc
 from paper_2607_04749_amd.workloads import WORKLOADS
@@ -61,7 +62,8 @@ def test_share_direct_refer(wl):
     keeps half of its state (its own layers) and receives the other half
     from one peer.  7B: it keeps its old shard, strided on both sides, and
     receives the rest from one peer.  13B: everything it needs is kept, so
-    the unpack has nothing to do."""
+    the unpack has nothing to do.  Every target and message byte against the
+    oracle's migration of the whole share under the same switch."""
     w = WORKLOADS[wl]
     pr = _sketch(w.model, w.src, w.dst)
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr, flags=etc.PLAN_DIRECT_REFER)
@@ -84,6 +86,8 @@ def test_share_direct_refer(wl):
     for s in feeders:
         n = check_send(plan, w.model, w.src, w.dst, s, send[s], w.seed, pair=pr, direct_refer=True)
         say(f"  send buffer of source {s}: {n} messages, every byte")
+    oracle_whole_check(w.model, w.src, w.dst, pr, src, feeders, d0, send, dst, direct_refer=True)
+    torch.cuda.empty_cache()
     say("  sampled origins")
     sampled_origin_check(w.model, w.src, w.dst, d0, dst, src, pair=pr)
     del send
