@@ -9,7 +9,7 @@ import torch
 
 import oracle
 from gpu_util import (DEV, ESIZE, alloc, check_chunks, emulate, equal, expected_dst, expected_send,
-                      say, seeded_arenas, to_dev)
+                      oracle_whole_check, say, seeded_arenas, to_dev)
 from helpers import empty_arenas as host_empty
 from helpers import host_arenas
 from micro import MICRO_MODELS, cfg_pairs
@@ -130,8 +130,9 @@ def test_share_chunked(wl):
     sketch also finds): every chunk buffer packed, byte for byte, against
     kind k's sections of the expected send buffer (the oracle's message
     boxes filled with the seeded values), and the whole target against the
-    seeded values.  70B is contiguous throughout; the 7B unpack and the 13B
-    pack copy strided rows."""
+    oracle's migration of the whole share and against the seeded values.
+    70B is contiguous throughout; the 7B unpack and the 13B pack copy
+    strided rows."""
     w = WORKLOADS[wl]
     pr = oracle.sketch(oracle.matrices(w.model, w.src, w.dst)["cost"])[0]
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr)
@@ -161,6 +162,7 @@ def test_share_chunked(wl):
         torch.cuda.empty_cache()
     del exp_send
     torch.cuda.empty_cache()
+    oracle_whole_check(w.model, w.src, w.dst, pr, src, [], d0, {}, dst)
     say("  full target vs seeded values")
     exp = expected_dst(w.model, w.dst, d0, w.seed)
     for k in range(4):

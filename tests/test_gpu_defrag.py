@@ -82,4 +82,4 @@ def test_llama_70b_share_coalesced_occupancy():
     got = device_matrices(plan)
     np.testing.assert_array_equal(got["route"],
                                   oracle.matrices(w.model, w.src, w.dst, pair=co)["route"])
-    share_run(dataclasses.replace(w, unpack_rank=8), plan, pair=co)
+    share_run(dataclasses.replace(w, unpack_rank=8), plan, pair=co, whole=True)
