@@ -14,8 +14,8 @@ and the new rank it becomes.
 With no --workload the run times the Llama-70B share (the line's value,
 roofline and CPU baseline) and then the Llama-7B share (under "shares", with
 its own rate, roofline and CPU baseline), each in a process of its own, as a
-deployment runs one migration per process: the two shares the 70 % target is
-stated on.  --workload NAME times that workload alone, in this process.
+deployment runs one migration per process.  --workload NAME times that
+workload alone, in this process.
 
 Modes: direct (default) packs and unpacks all four state kinds in one launch
 each; chunked moves one state kind at a time through per-kind chunk buffers
@@ -475,7 +475,7 @@ def main():
         sys.exit(2)
 
     if not args.workload:
-        # Both gated shares, each in a process of its own (one migration per
+        # The 70B and 7B shares, each in a process of its own (one migration per
         # process, as deployed), the 70B share first; this process makes no
         # GPU call, so none forks with GPU state.
         outs = {}
