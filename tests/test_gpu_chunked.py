@@ -218,3 +218,17 @@ def test_gpt_1_3b_chunked_eager_release_memory():
     full_peak = torch.cuda.max_memory_allocated() - base
     say(f"  one-shot peak {full_peak / 1e9:.2f} GB = {full_peak / src_bytes:.3f} x")
     assert chunked_peak < 0.6 * full_peak
+
+
+RANDOM_CASES = __import__("randcfg").cases(16, base=0xC4A1)
+
+
+@pytest.mark.parametrize("i", range(len(RANDOM_CASES)))
+def test_random_chunked_against_oracle(i):
+    """State chunking on seeded random shapes and configurations (ragged
+    boxes, launches of a few tiles, where most windows of the one-kind walk
+    are empty): every target byte and every chunk message against the
+    oracle."""
+    m, a, b = RANDOM_CASES[i]
+    say("random chunked case", i, m, a, "->", b)
+    _compare_with_oracle(m, a, b, 0xC4A1 + i)
