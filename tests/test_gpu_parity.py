@@ -148,14 +148,13 @@ def test_share_at_full_size(wl, pairing):
     Every send buffer packed is compared in full: the 13B source 0 packs
     messages to targets 0 and 1, and under the identity pairing also the
     norms message to target 4.  The oracle's own migration of the whole
-    share checks every target and message byte in the benchmark's
-    configuration, and under the identity pairing at 13B."""
+    share checks every target and message byte under both pairings."""
     w = WORKLOADS[wl]
     pr = oracle_sketch(w) if pairing == "sketch" else None
     say(wl, "share", w.src, "->", w.dst, pairing, "process", w.pack_rank)
     plan = etc.etc_plan(w.model, w.src, w.dst, pair=pr)
     check_matrices(plan, w.model, w.src, w.dst, pr)
-    share_run(w, plan, pair=pr, whole=pairing == "sketch" or wl == "llama-13b")
+    share_run(w, plan, pair=pr, whole=True)
 
 
 def test_max_peers_full_emulation():
