@@ -151,6 +151,16 @@ __global__ __launch_bounds__(kSubThreads) void copy_kind_kernel(CopyArgs a) {
   }
 }
 
+// LDS reserved per workgroup of an all-kinds launch and never touched: with
+// 160 KB of LDS per CU it lets at most 25 of these one-wave workgroups share
+// a CU, where they would otherwise fill its 32 wave slots.  The copy keeps
+// HBM's queues full either way.  With fewer requests queued, MI355X ran the
+// 70B and 7B shares 2-3 % faster in their slower buffer placements, and
+// every other all-kinds launch measured within -1 to +1.6 %.  A cap of 21
+// workgroups ran 1-3.5 % below the cap of 25.  One-kind launches, whose
+// workgroups move 8 KB each, lost with any cap and keep all 32 slots.
+constexpr unsigned kSubLdsBytes = 6400;
+
 }  // namespace
 
 hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t ntiles, uint32_t kind_mask,
@@ -171,9 +181,9 @@ hipError_t launch_copy(bool pack, const CopyBox* boxes, uint32_t nbox, uint32_t 
   for (int p = 0; p < npeers; ++p) a.peer[p] = static_cast<char*>(peers[p]);
   const dim3 grid = dim3(uint32_t(nwg)), block = dim3(kSubThreads);
   if (all && pack)
-    hipLaunchKernelGGL((copy_sub_kernel<true>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((copy_sub_kernel<true>), grid, block, kSubLdsBytes, stream, a);
   else if (all)
-    hipLaunchKernelGGL((copy_sub_kernel<false>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((copy_sub_kernel<false>), grid, block, kSubLdsBytes, stream, a);
   else if (pack)
     hipLaunchKernelGGL((copy_kind_kernel<true>), grid, block, 0, stream, a);
   else
