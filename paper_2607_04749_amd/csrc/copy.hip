@@ -18,7 +18,8 @@
 // Either way a workgroup finds its tile's descriptor once (a binary search of
 // the tile table, scalar loads) and then moves a few KB.  The hardware
 // dispatches the workgroups in index order, so the whole GPU advances
-// through each buffer as one compact front.  On MI355X this ran 5-14 %
+// through each buffer as one compact front; an all-kinds launch reserves
+// LDS so that at most 25 of its workgroups share a CU (kSubLdsBytes).  On MI355X this ran 5-14 %
 // faster than a persistent grid of one deep-batched workgroup per CU for all
 // four kinds, and up to 9 % faster for one kind, and it holds its rate where
 // the persistent grid lost about 10 % to an unfavourable relative placement
