@@ -11,7 +11,7 @@ from randcfg import cases
 
 pytestmark = pytest.mark.gpu
 
-GPU_CASES = cases(24)
+GPU_CASES = cases(200)
 
 
 @pytest.fixture(autouse=True)
@@ -33,7 +33,7 @@ def test_random_full_emulation(i):
     full_compare(m, a, b, 0x5EED + i, pair=sk, round_trip=False)
 
 
-DP_FAIL_CASES = [c for c in cases(200, base=0xD9) if c[1].dp > 1][:8]
+DP_FAIL_CASES = [c for c in cases(400, base=0xD9) if c[1].dp > 1][:40]
 
 
 @pytest.mark.parametrize("i", range(len(DP_FAIL_CASES)))
