@@ -220,7 +220,7 @@ def test_gpt_1_3b_chunked_eager_release_memory():
     assert chunked_peak < 0.6 * full_peak
 
 
-RANDOM_CASES = __import__("randcfg").cases(16, base=0xC4A1)
+RANDOM_CASES = __import__("randcfg").cases(64, base=0xC4A1)
 
 
 @pytest.mark.parametrize("i", range(len(RANDOM_CASES)))
