@@ -7,7 +7,7 @@ import torch
 
 import oracle
 from gpu_util import full_compare, say
-from randcfg import cases
+from randcfg import cases, medium_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -49,3 +49,23 @@ def test_random_failed_rank_full_emulation(i):
     sk, _ = oracle.sketch(C)
     sk = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)], np.int32)
     full_compare(m, a, b, 0xFA11 + i, pair=sk, failed=failed, round_trip=False, direct_refer=True)
+
+
+MEDIUM_CASES = medium_cases(48)
+
+
+@pytest.mark.parametrize("i", range(len(MEDIUM_CASES)))
+def test_medium_random_full_emulation(i):
+    """Medium random shapes (randcfg.medium_case: boxes of several tiles with
+    ragged tails, odd widths, uneven TP ratios): every message and target
+    byte against the oracle, under the identity pairing with a round trip
+    for even cases and under the oracle's sketch for odd ones."""
+    m, a, b = MEDIUM_CASES[i]
+    say("medium random case", i, m, a, "->", b)
+    if i % 2 == 0:
+        full_compare(m, a, b, 0x3ED0 + i)
+        return
+    C = oracle.matrices(m, a, b)["cost"]
+    sk, _ = oracle.sketch(C)
+    sk = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)], np.int32)
+    full_compare(m, a, b, 0x3ED0 + i, pair=sk, round_trip=False)

@@ -17,7 +17,7 @@ import pytest
 import oracle
 from micro import MICRO_MODELS, cfg_pairs
 from paper_2607_04749_amd.workloads import WORKLOADS, Parallel as P
-from randcfg import cases
+from randcfg import cases, medium_cases
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2607_04749_amd", "csrc")
@@ -121,6 +121,17 @@ def test_coalesced_pairings(tilewalk):
 def test_random_configurations(tilewalk):
     jobs = []
     for m, a, b in cases(48):
+        jobs.append(_args(m, a, b, False, "identity"))
+        jobs.append(_args(m, a, b, True, _oracle_sketch(m, a, b)))
+    _run_all(tilewalk, jobs)
+
+
+def test_medium_random_configurations(tilewalk):
+    """Boxes of several tiles with ragged tails and odd widths (randcfg's
+    medium shapes), under the identity pairing and the oracle's sketch with
+    direct Refer."""
+    jobs = []
+    for m, a, b in medium_cases(48):
         jobs.append(_args(m, a, b, False, "identity"))
         jobs.append(_args(m, a, b, True, _oracle_sketch(m, a, b)))
     _run_all(tilewalk, jobs)
