@@ -232,3 +232,16 @@ def test_random_chunked_against_oracle(i):
     m, a, b = RANDOM_CASES[i]
     say("random chunked case", i, m, a, "->", b)
     _compare_with_oracle(m, a, b, 0xC4A1 + i)
+
+
+MEDIUM_CASES = __import__("randcfg").medium_cases(16, base=0xC4B0)
+
+
+@pytest.mark.parametrize("i", range(len(MEDIUM_CASES)))
+def test_medium_chunked_against_oracle(i):
+    """State chunking on medium random shapes (one-kind launches over boxes
+    of several tiles, with ragged tails and odd widths): every target byte
+    and every chunk message against the oracle."""
+    m, a, b = MEDIUM_CASES[i]
+    say("medium chunked case", i, m, a, "->", b)
+    _compare_with_oracle(m, a, b, 0xC4B0 + i)

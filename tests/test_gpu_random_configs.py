@@ -59,7 +59,8 @@ def test_medium_random_full_emulation(i):
     """Medium random shapes (randcfg.medium_case: boxes of several tiles with
     ragged tails, odd widths, uneven TP ratios): every message and target
     byte against the oracle, under the identity pairing with a round trip
-    for even cases and under the oracle's sketch for odd ones."""
+    for even cases and under the oracle's sketch, with and without direct
+    Refer, for odd ones."""
     m, a, b = MEDIUM_CASES[i]
     say("medium random case", i, m, a, "->", b)
     if i % 2 == 0:
@@ -69,3 +70,4 @@ def test_medium_random_full_emulation(i):
     sk, _ = oracle.sketch(C)
     sk = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)], np.int32)
     full_compare(m, a, b, 0x3ED0 + i, pair=sk, round_trip=False)
+    full_compare(m, a, b, 0x3ED0 + i, pair=sk, round_trip=False, direct_refer=True)
