@@ -2,7 +2,8 @@
 6, PP 1-4, DP 1-2, GPT and Llama, tied or untied, heads of width 1-4): the
 oracle's brute force equals its item form, every target receives exactly its
 bytes, and the library planner agrees with the oracle on layouts, message
-layouts and routing, under the identity pairing and under the sketch."""
+layouts and routing, under the identity pairing and under the sketch; the
+same for medium shapes (randcfg.medium_case)."""
 import numpy as np
 import pytest
 
@@ -10,7 +11,7 @@ import oracle
 from helpers import rank_elems
 from paper_2607_04749_amd import etc
 from paper_2607_04749_amd.workloads import Parallel
-from randcfg import cases
+from randcfg import cases, medium_cases
 
 HOST = etc.PLAN_HOST_ONLY
 CASES = cases(240)
@@ -29,7 +30,20 @@ def dp_bytes(m, cfg, r):
 
 @pytest.mark.parametrize("i", range(len(CASES)))
 def test_random_case(i):
-    m, a, b = CASES[i]
+    _check_case(*CASES[i])
+
+
+MEDIUM = medium_cases(48)
+
+
+@pytest.mark.parametrize("i", range(len(MEDIUM)))
+def test_medium_random_case(i):
+    """The same on randcfg's medium shapes (boxes of several tiles, odd
+    widths, uneven TP ratios; too large for the brute force)."""
+    _check_case(*MEDIUM[i])
+
+
+def _check_case(m, a, b):
     I = oracle.matrices(m, a, b)
     if sum(dp_bytes(m, a, s) for s in range(a.world)) < 14 * 200_000:
         B = oracle.matrices(m, a, b, brute=True)
