@@ -247,6 +247,14 @@ def run_share(w, args):
             flags |= etc.PLAN_DIRECT_REFER
         plan = etc.etc_plan(w.model, w.src, w.dst, flags=flags)
     plan_ms = (time.perf_counter() - t0) * 1e3
+    # what one process of a deployment pays: a plan with only its own
+    # launches' tables (the kernels are loaded by now)
+    plan_process_ms = None
+    if w.mode != "full" and moved is None:
+        t1 = time.perf_counter()
+        mine = etc.etc_plan(w.model, w.src, w.dst, rank=w.pack_rank, flags=flags)
+        plan_process_ms = (time.perf_counter() - t1) * 1e3
+        mine.free()
     S, D = plan.S, plan.D
     if w.mode == "full":  # every source packs, every target unpacks
         packers, unpackers = list(range(S)), list(range(D))
@@ -440,6 +448,7 @@ def run_share(w, args):
         "cost_matrix_us": round(cm_us, 2), "cost_matrix_cells": S * D,
         "sketch_us": round(sketch_us, 1), "pairing": pairing,
         "d2d_copy_GBps": round(d2d_gbps, 1), "plan_ms": round(plan_ms, 2),
+        "plan_process_ms": None if plan_process_ms is None else round(plan_process_ms, 2),
         "roofline": {"bound": "hbm", "kernel": kernel,
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
@@ -460,7 +469,7 @@ def run_share(w, args):
 
 SHARE_KEYS = ("value", "unit", "ms_per_step", "frac_of_peak", "pack_GBps", "unpack_GBps", "pack_ms",
               "unpack_ms", "pack_bytes", "unpack_bytes", "launches_per_step", "cost_matrix_us",
-              "cost_matrix_cells", "sketch_us", "pairing", "d2d_copy_GBps", "plan_ms", "roofline",
+              "cost_matrix_cells", "sketch_us", "pairing", "d2d_copy_GBps", "plan_ms", "plan_process_ms", "roofline",
               "refer_GBps", "refer_ms", "refer_bytes")
 
 
