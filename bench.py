@@ -50,7 +50,6 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
 METRIC = "pack+unpack HBM GB/s per GPU (fraction of peak) + cost-matrix time"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "copy_kernel_traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_04749_amd", "csrc", "copy.hip")
 
 
 def log(*a):
@@ -469,8 +468,8 @@ def run_share(w, args):
 
 SHARE_KEYS = ("value", "unit", "ms_per_step", "frac_of_peak", "pack_GBps", "unpack_GBps", "pack_ms",
               "unpack_ms", "pack_bytes", "unpack_bytes", "launches_per_step", "cost_matrix_us",
-              "cost_matrix_cells", "sketch_us", "pairing", "d2d_copy_GBps", "plan_ms", "plan_process_ms", "roofline",
-              "refer_GBps", "refer_ms", "refer_bytes")
+              "cost_matrix_cells", "sketch_us", "pairing", "d2d_copy_GBps", "plan_ms", "plan_process_ms",
+              "roofline", "refer_GBps", "refer_ms", "refer_bytes")
 
 
 def main():
