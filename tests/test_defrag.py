@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 from helpers import rank_elems
-from micro import MICRO_MODELS, cfg_pairs, layers_only
+from micro import MICRO_MODELS, layers_only
 from paper_2607_04749_amd import etc
 from paper_2607_04749_amd.workloads import Parallel
 

@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import synth
-from helpers import (ESIZE, empty_arenas, full_cols, host_arenas, lcm, rank_elems, send_bufs,
+from helpers import (ESIZE, empty_arenas, host_arenas, lcm, rank_elems, send_bufs,
                      unique_params)
 from micro import MICRO_MODELS, cfg_pairs, layers_only
 from paper_2607_04749_amd.workloads import GPT, WORKLOADS, Parallel

@@ -8,7 +8,6 @@ element; and on small models the brute-force matrices equal the item form."""
 import math
 
 import numpy as np
-import pytest
 from hypothesis import HealthCheck, given, settings
 from hypothesis import strategies as st
 
