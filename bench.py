@@ -9,7 +9,7 @@ pairs rank d with rank d); the share is process 0's: the old rank it packs
 and the new rank it becomes.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
-                    [--identity] [--mode direct|chunked|coalesced|refer]
+                    [--identity] [--mode direct|chunked|coalesced|refer|failover]
 
 With no --workload the run times the Llama-70B share (the line's value,
 roofline and CPU baseline) and then the Llama-7B share (under "shares", with
@@ -25,7 +25,11 @@ de-fragmentation (Sec. III-E) and times the share of the first process that
 takes over a moved rank, which receives that rank's whole state; refer keeps
 the data a target's paired source holds on the GPU (Refer, Sec. III-D): it is
 copied arena to arena and travels in no message, so the step is the refer
-copy, the pack of what leaves and the unpack of what arrives.
+copy, the pack of what leaves and the unpack of what arrives; failover runs
+the workload with two replicas of each configuration and old rank 0 lost
+(Sec. III-C): new rank 0 gets that rank's part from the other replica, and
+the step is that replica source's pack (for its own replica's target and for
+new rank 0) and new rank 0's unpack.
 
 Prints one JSON line: value = algorithmic bytes of pack + unpack (each reads
 and writes its routed bytes) per step time, in GB/s; the roofline object is for
@@ -36,6 +40,7 @@ and on up to 16 threads (reported).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import gc
 import hashlib
 import json
@@ -210,7 +215,7 @@ def parse_args():
                     help="one workload alone (default: the 70B share, then the 7B share)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--identity", action="store_true", help="identity pairing instead of the sketch")
-    ap.add_argument("--mode", choices=("direct", "chunked", "coalesced", "refer"), default="direct")
+    ap.add_argument("--mode", choices=("direct", "chunked", "coalesced", "refer", "failover"), default="direct")
     return ap.parse_args()
 
 
@@ -222,11 +227,15 @@ def run_share(w, args):
 
     import synth
     from paper_2607_04749_amd import etc
-    from paper_2607_04749_amd.workloads import ESIZE
+    from paper_2607_04749_amd.workloads import ESIZE, Parallel
 
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     pairing = "identity" if args.identity else ("coalesced" if args.mode == "coalesced" else "sketch")
+    failed = None
+    if args.mode == "failover":  # two replicas of each configuration; old rank 0 is lost
+        w = dataclasses.replace(w, src=Parallel(w.src.tp, w.src.pp, 2), dst=Parallel(w.dst.tp, w.dst.pp, 2))
+        failed = [0]
 
     t0 = time.perf_counter()
     moved = None
@@ -244,12 +253,12 @@ def run_share(w, args):
         flags = 0 if args.identity else etc.PLAN_SKETCH
         if args.mode == "refer":
             flags |= etc.PLAN_DIRECT_REFER
-        plan = etc.etc_plan(w.model, w.src, w.dst, flags=flags)
+        plan = etc.etc_plan(w.model, w.src, w.dst, flags=flags, failed=failed)
     plan_ms = (time.perf_counter() - t0) * 1e3
     # what one process of a deployment pays: a plan with only its own
     # launches' tables (the kernels are loaded by now)
     plan_process_ms = None
-    if w.mode != "full" and moved is None:
+    if w.mode != "full" and moved is None and failed is None:
         t1 = time.perf_counter()
         mine = etc.etc_plan(w.model, w.src, w.dst, rank=w.pack_rank, flags=flags)
         plan_process_ms = (time.perf_counter() - t1) * 1e3
@@ -259,6 +268,15 @@ def run_share(w, args):
         packers, unpackers = list(range(S)), list(range(D))
     elif moved is not None:  # the process that takes over a moved rank
         packers, unpackers = [moved[0]], [moved[1]]
+    elif failed is not None:
+        # new rank 0, whose paired old rank is lost, and the other replica's
+        # source that now sends it that rank's part (besides its own replica's)
+        counts = plan.recv_counts(w.unpack_rank)
+        half = S // 2
+        partner = max(range(half, S), key=lambda s: int(counts[s]))
+        if not counts[partner]:
+            raise SystemExit(f"{w.name}: no source of the second replica feeds target {w.unpack_rank}")
+        packers, unpackers = [partner], [w.unpack_rank]
     else:  # process 0's share: the old rank it packs, the new rank it becomes
         s0, d0 = plan.process(w.pack_rank)
         if d0 < 0:
@@ -432,8 +450,12 @@ def run_share(w, args):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: {w.note}", "src": f"TP{w.src.tp}xPP{w.src.pp}",
-                   "dst": f"TP{w.dst.tp}xPP{w.dst.pp}", "mode": args.mode,
+        "config": {"workload": f"{w.name}: {w.note}" if not failed else
+                   (f"{w.name}: TP{w.src.tp}xPP{w.src.pp} -> TP{w.dst.tp}xPP{w.dst.pp}, two replicas each, "
+                    f"old rank 0 lost, pack old rank {packers[0]}, unpack new rank {unpackers[0]}"),
+                   "src": f"TP{w.src.tp}xPP{w.src.pp}" + (f"xDP{w.src.dp}" if w.src.dp > 1 else ""),
+                   "dst": f"TP{w.dst.tp}xPP{w.dst.pp}" + (f"xDP{w.dst.dp}" if w.dst.dp > 1 else ""),
+                   "mode": args.mode, "failed_ranks": failed or [],
                    "pairing": {"identity": "identity", "sketch": "migration sketch",
                                "coalesced": "coalesced (sketch + occupancy de-fragmentation)"}[pairing],
                    "refer": "arena to arena (direct)" if args.mode == "refer" else "through a message",
@@ -514,7 +536,9 @@ def main():
     gc.collect()
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
+    if args.mode == "failover":
+        log(f"{w.name}: no cpu baseline in failover mode (the oracle sample follows the default share)")
+    elif not args.no_cpu_baseline:
         log(f"{w.name}: cpu baseline (oracle) ...")
         line["cpu_baseline"] = cpu_baseline(w, pairing, direct_refer=args.mode == "refer")
     print(json.dumps(line), flush=True)

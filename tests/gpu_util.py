@@ -245,7 +245,7 @@ def check_chunks(plan, model, src, dst, s, k, chunk, exp_send):
 
 
 def oracle_whole_check(model, src, dst, pair, dev_src, packed, d0, dev_send, dev_dst, threads=16,
-                       direct_refer=False):
+                       direct_refer=False, failed=None):
     """The oracle's own migration of a whole share at real shape, against the
     GPU's: the resident sources (from the seeded generator, copied from the
     device) are materialized and cut one logical tensor per thread (the
@@ -255,13 +255,13 @@ def oracle_whole_check(model, src, dst, pair, dev_src, packed, d0, dev_send, dev
     from concurrent.futures import ThreadPoolExecutor
     hs = {s: [x.cpu().numpy() for x in ar] for s, ar in dev_src.items()}
     hd = [np.zeros(x.numel(), np.uint8) for x in dev_dst]
-    hb = {s: np.zeros(max(oracle.send_layout(model, src, dst, s, pair=pair, direct_refer=direct_refer)[3], 1),
-                      np.uint8) for s in packed}
+    hb = {s: np.zeros(max(oracle.send_layout(model, src, dst, s, pair=pair, failed=failed,
+                                             direct_refer=direct_refer)[3], 1), np.uint8) for s in packed}
     nt = len(oracle.tensors(model))
     say(f"  the oracle: {nt} tensors on {threads} threads")
     with ThreadPoolExecutor(threads) as ex:
         list(ex.map(lambda t: oracle.migrate(model, src, dst, hs, {d0: hd}, hb, t, t + 1, pair=pair,
-                                             direct_refer=direct_refer), range(nt)))
+                                             failed=failed, direct_refer=direct_refer), range(nt)))
     del hs
     for k in range(4):
         assert equal(dev_dst[k], torch.from_numpy(hd[k]).to(DEV)), f"target {d0} kind {k} vs the oracle"

@@ -33,8 +33,9 @@ def test_traffic_record_matches_the_kernel():
     kinds = {bench.launch_key("chunked", side, k) for side in ("pack", "unpack") for k in range(4)}
     need = {
         "llama-70b": {"direct/pack", "direct/unpack", "refer/refer", "refer/unpack", "coalesced/pack",
-                      "coalesced/unpack"} | kinds,
-        "llama-7b": {"direct/pack", "direct/unpack", "refer/refer", "refer/unpack"} | kinds,
+                      "coalesced/unpack", "failover/pack", "failover/unpack"} | kinds,
+        "llama-7b": {"direct/pack", "direct/unpack", "refer/refer", "refer/unpack", "failover/pack",
+                     "failover/unpack"} | kinds,
         "llama-13b": {"direct/pack", "direct/unpack", "refer/refer", "refer/pack"} | kinds,
         "gpt-1.3b": {"direct/pack", "direct/unpack"} | kinds,
     }

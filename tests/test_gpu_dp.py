@@ -83,3 +83,47 @@ def test_large_dp_cost_matrices():
     check_matrices(sk, w.model, a, b, pair=sk.pairing(), failed=failed)
     ident = etc.etc_plan(w.model, a, b, failed=failed)
     check_matrices(ident, w.model, a, b, pair=None, failed=failed)
+
+
+@pytest.mark.parametrize("wl", ["llama-7b", "llama-70b"])
+def test_share_failover_at_full_size(wl):
+    """The failover share that bench.py --mode failover times: two replicas of
+    each configuration, old rank 0 lost, the oracle's sketch.  New rank 0 gets
+    the lost rank's part from its partner in the other replica.  Every byte
+    of new rank 0's arenas and of the partner's send buffer against the
+    oracle's own migration at real shape, every resident source's send buffer
+    against the oracle's message boxes, and the target against the seeded
+    values."""
+    from gpu_util import alloc, check_send, equal, expected_dst, oracle_whole_check, seeded_arenas
+    w = WORKLOADS[wl]
+    a, b = P(w.src.tp, w.src.pp, 2), P(w.dst.tp, w.dst.pp, 2)
+    failed, d0 = [0], 0
+    C = oracle.matrices(w.model, a, b, failed=failed)["cost"]
+    sk, _ = oracle.sketch(C)
+    sk = np.array([p if p >= 0 and C[d, p] < oracle.COST_INF else -1 for d, p in enumerate(sk)], np.int32)
+    plan = etc.etc_plan(w.model, a, b, pair=sk, failed=failed)
+    counts = plan.recv_counts(d0)
+    assert not counts[failed[0]], "a lost rank sends nothing"
+    partner = max(range(a.world // 2, a.world), key=lambda s: int(counts[s]))
+    assert counts[partner], "the other replica feeds the lost rank's target"
+    resident = sorted({int(s) for s in np.nonzero(counts)[0]} | {partner})
+    say(wl, a, "->", b, "failed", failed, "partner", partner, "resident", resident)
+    ds = seeded_arenas(w.model, a, resident, w.seed)
+    send = {}
+    for s in resident:
+        send[s] = torch.zeros(max(plan.send_layout(s)[3], 256), dtype=torch.uint8, device="cuda:0")
+        etc.etc_pack(plan, s, ds[s], send[s])
+    msgs = [send[s].data_ptr() + int(plan.send_layout(s)[2][d0]) if s in send and plan.send_layout(s)[0][d0]
+            else None for s in range(a.world)]
+    dd = alloc(plan.arena_elems(etc.SIDE_DST, d0))
+    etc.etc_unpack(plan, d0, msgs, dd)
+    torch.cuda.synchronize()
+    for s in resident:
+        n = check_send(plan, w.model, a, b, s, send[s][:plan.send_layout(s)[3]], w.seed, pair=sk, failed=failed)
+        say(f"  send buffer of source {s}: {n} messages, every byte")
+    oracle_whole_check(w.model, a, b, sk, ds, [partner], d0, send, dd, failed=failed)
+    del send
+    torch.cuda.empty_cache()
+    exp = expected_dst(w.model, b, d0, w.seed)
+    for k in range(4):
+        assert equal(dd[k], exp[k]), f"target {d0} kind {k}"
